@@ -1,0 +1,275 @@
+"""Pins for the fp64 oracle: checks against values that do not come from the
+oracle itself.  Each function takes an optional ctypes library so that the
+mutation tests can run the same pins against planted-bug builds of oracle.c.
+
+Sources of truth used here:
+  * a hand-worked example (tests/golden/*.json), derived on paper from
+    Eq. gated-MLP and Eq. drelu of Turbo Sparse (arXiv 2406.05955);
+  * exact rational arithmetic (fractions.Fraction) on tiny inputs, with the
+    oracle required to sit inside the fp64 forward-error bound of a
+    recursively summed dot product, |fl(s) - s| <= gamma_n * sum|terms|,
+    gamma_n = n u / (1 - n u), u = 2^-53 (Higham, Accuracy and Stability of
+    Numerical Algorithms, section 3.1), propagated through the ReLU products;
+  * special cases that reduce to a library routine (numpy matmul, softmax);
+  * exact invariants (skipping the zero Combined activations changes no bit).
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+from decimal import Decimal, getcontext
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+from paper_2406_05955_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+U = 2.0 ** -53
+
+
+def gamma(n: int) -> float:
+    return n * U / (1.0 - n * U)
+
+
+def _load_golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _f32(a):
+    return np.asarray(a, dtype=np.float32)
+
+
+# ----------------------------------------------------------------------------
+# Hand-worked examples
+
+
+def pin_ffn_handworked(lib=None):
+    gd = _load_golden("ffn_handworked.json")
+    r = oracle.ffn(_f32(gd["x"]), _f32(gd["w_gate"]), _f32(gd["w_up"]), _f32(gd["w_down_t"]),
+                   oracle.F32, threads=1, lib=lib)
+    assert np.array_equal(r.y, np.asarray(gd["out"], np.float64)), r.y
+    assert np.array_equal(r.g, np.asarray(gd["gate"], np.float64)), r.g
+    assert np.array_equal(r.u, np.asarray(gd["up"], np.float64)), r.u
+    for t in range(2):
+        assert r.gate_set(t).tolist() == gd["gate_set"][t]
+        assert r.active_set(t).tolist() == gd["active_set"][t]
+
+
+def _moe_golden_inputs():
+    f = _load_golden("ffn_handworked.json")
+    m = _load_golden("moe_handworked.json")
+    wg1 = _f32(f["w_gate"])
+    wu1 = _f32(f["w_up"])
+    wd1 = _f32(f["w_down_t"])
+    wg = np.stack([wg1, wg1, wg1])
+    wu = np.stack([wu1, wu1, wu1])
+    wd = np.stack([wd1, 2 * wd1, np.full_like(wd1, 100.0)])
+    return _f32(m["x"]), _f32(m["w_router"]), wg, wu, wd, m
+
+
+def pin_moe_handworked(lib=None):
+    x, wr, wg, wu, wd, m = _moe_golden_inputs()
+    r = oracle.moe(x, wr, wg, wu, wd, oracle.F32, top_k=2, threads=1, lib=lib)
+    assert r.topk_idx.tolist() == m["topk_idx"], r.topk_idx
+    rr = 1.0 / (1.0 + math.e)
+    assert np.allclose(r.topk_w[0], [0.5, 0.5], rtol=0, atol=0), r.topk_w
+    assert np.allclose(r.topk_w[1], [1 - rr, rr], rtol=4 * U, atol=0), r.topk_w
+    assert np.array_equal(r.y[0], [3.0, 18.0, 6.0]), r.y
+    want1 = np.array([4.0, 2.0, -3.0]) * (1.0 + rr)
+    assert np.allclose(r.y[1], want1, rtol=16 * U, atol=0), (r.y[1], want1)
+
+
+# ----------------------------------------------------------------------------
+# Exact rational brute force
+
+
+def _exact_ffn_token(x, wg, wu, wd):
+    """x [H], w* [I][H] as Fractions.  Returns exact (g, u, h, y) and the
+    per-element forward-error bound of a fp64 evaluation in the oracle's
+    order."""
+    I, H = len(wg), len(x)
+    g = [sum((wg[i][j] * x[j] for j in range(H)), Fraction(0)) for i in range(I)]
+    u = [sum((wu[i][j] * x[j] for j in range(H)), Fraction(0)) for i in range(I)]
+    h = [g[i] * u[i] if (g[i] > 0 and u[i] > 0) else Fraction(0) for i in range(I)]
+    y = [sum((wd[i][j] * h[i] for i in range(I)), Fraction(0)) for j in range(H)]
+    eg = [gamma(H) * float(sum(abs(wg[i][j] * x[j]) for j in range(H))) for i in range(I)]
+    eu = [gamma(H) * float(sum(abs(wu[i][j] * x[j]) for j in range(H))) for i in range(I)]
+    eh = []
+    for i in range(I):
+        ag, au = abs(float(g[i])), abs(float(u[i]))
+        # relu is 1-Lipschitz; the product adds one rounding.
+        eh.append((ag + eg[i]) * eu[i] + au * eg[i] + U * (ag + eg[i]) * (au + eu[i]))
+    ey = []
+    for j in range(H):
+        s_abs = sum(abs(float(wd[i][j])) * (abs(float(h[i])) + eh[i]) for i in range(I))
+        ey.append(gamma(I) * s_abs + sum(abs(float(wd[i][j])) * eh[i] for i in range(I)))
+    return g, u, h, y, ey
+
+
+def _as_fractions(a, dtype):
+    vals = synth.bf16_bits_to_f32(a) if dtype == synth.BF16 else np.asarray(a, np.float32)
+    return [[Fraction(float(v)) for v in row] for row in np.atleast_2d(vals)]
+
+
+def _within(yhat: float, y: Fraction, bound: float) -> bool:
+    return float(abs(Fraction(yhat) - y)) <= 1.5 * bound + 1e-300
+
+
+BRUTE_SHAPES = [(1, 1, 1), (1, 2, 5), (3, 3, 1), (2, 8, 16), (1, 5, 3), (3, 4, 7)]
+
+
+def pin_ffn_bruteforce(lib=None):
+    for dtype in (synth.F32, synth.BF16):
+        for k, (B, H, I) in enumerate(BRUTE_SHAPES):
+            for bias in (-0.3, 0.4):
+                inp = synth.make_ffn(B, H, I, gate_bias=bias, dtype=dtype, seed=[17, k, dtype],
+                                     bias_feature=H > 1)
+                r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, threads=1, lib=lib)
+                wg, wu, wd = (_as_fractions(w, dtype) for w in (inp.w_gate, inp.w_up, inp.w_down_t))
+                for t in range(B):
+                    x = [Fraction(float(v)) for v in inp.x[t]]
+                    g, u, h, y, ey = _exact_ffn_token(x, wg, wu, wd)
+                    for j in range(H):
+                        assert _within(r.y[t, j], y[j], ey[j]), (dtype, B, H, I, t, j, r.y[t, j], float(y[j]))
+                    for i in range(I):
+                        assert _within(r.g[t, i], g[i], gamma(H) * sum(abs(float(wg[i][j] * x[j])) for j in range(H)))
+                        assert _within(r.u[t, i], u[i], gamma(H) * sum(abs(float(wu[i][j] * x[j])) for j in range(H)))
+
+
+def _dec(fr: Fraction) -> Decimal:
+    return Decimal(fr.numerator) / Decimal(fr.denominator)
+
+
+def pin_moe_bruteforce(lib=None):
+    getcontext().prec = 60
+    cases = [(1, 4, 5, 1, 1), (2, 4, 6, 4, 2), (3, 3, 4, 3, 3), (2, 6, 3, 4, 1), (1, 8, 5, 2, 2)]
+    for dtype in (synth.F32, synth.BF16):
+        for k, (B, H, I, E, K) in enumerate(cases):
+            inp = synth.make_moe(B, H, I, E, K, gate_bias=0.0, dtype=dtype, seed=[23, k, dtype])
+            r = oracle.moe(inp.x, inp.w_router, inp.w_gate, inp.w_up, inp.w_down_t, dtype, K, threads=1,
+                           lib=lib)
+            wr = _as_fractions(inp.w_router, dtype)
+            experts = [tuple(_as_fractions(w[e], dtype) for w in (inp.w_gate, inp.w_up, inp.w_down_t))
+                       for e in range(E)]
+            for t in range(B):
+                x = [Fraction(float(v)) for v in inp.x[t]]
+                logits = [sum((wr[e][j] * x[j] for j in range(H)), Fraction(0)) for e in range(E)]
+                m = max(logits)
+                p = [(_dec(l - m)).exp() for l in logits]
+                z = sum(p)
+                p = [pe / z for pe in p]
+                order = sorted(range(E), key=lambda e: (-logits[e], e))
+                sel = order[:K]
+                # Skip tokens whose k-th and (k+1)-th logits tie within fp64 error.
+                if K < E and abs(float(logits[order[K - 1]] - logits[order[K]])) < 1e-12:
+                    continue
+                assert r.topk_idx[t].tolist() == sel, (r.topk_idx[t], sel)
+                psel = sum(p[e] for e in sel)
+                w = {e: p[e] / psel for e in sel}
+                for kk, e in enumerate(sel):
+                    assert abs(Decimal(float(r.topk_w[t, kk])) - w[e]) <= Decimal(1e-14), (r.topk_w[t], w)
+                    assert abs(Decimal(float(r.probs[t, e])) - p[e]) <= Decimal(1e-14)
+                ys = {e: _exact_ffn_token(x, *experts[e]) for e in sel}
+                for j in range(H):
+                    want = sum(w[e] * _dec(ys[e][3][j]) for e in sorted(sel))
+                    tol = sum(float(w[e]) * 1.5 * ys[e][4][j] + 1e-14 * abs(float(ys[e][3][j])) for e in sel)
+                    assert abs(float(Decimal(float(r.y[t, j])) - want)) <= tol + 1e-300, (t, j, r.y[t, j], want)
+
+
+# ----------------------------------------------------------------------------
+# Special cases and invariants
+
+
+def pin_ffn_zero_bias(lib=None):
+    inp = synth.make_ffn(2, 64, 96, gate_bias=-100.0, dtype=synth.F32, seed=5)
+    r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, oracle.F32, lib=lib)
+    assert np.all(r.y == 0.0)
+    assert r.n_gate.tolist() == [0, 0] and r.n_active.tolist() == [0, 0]
+
+
+def pin_ffn_all_active_numpy(lib=None):
+    inp = synth.make_ffn(3, 48, 80, gate_bias=100.0, dtype=synth.F32, seed=6)
+    inp.w_up[:, 0] = 100.0
+    r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, oracle.F32, lib=lib)
+    x = inp.x.astype(np.float64)
+    g = x @ inp.w_gate.astype(np.float64).T
+    u = x @ inp.w_up.astype(np.float64).T
+    assert np.all(g > 0) and np.all(u > 0)
+    y = (g * u) @ inp.w_down_t.astype(np.float64)
+    assert np.allclose(r.y, y, rtol=1e-12, atol=1e-12 * np.abs(y).max())
+    assert r.n_active.tolist() == [80, 80, 80]
+
+
+def pin_ffn_sets_numpy(lib=None):
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 256, 700, gate_bias=-0.84, dtype=dtype, seed=7)
+        r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, lib=lib)
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        x = inp.x.astype(np.float64)
+        g = x @ up(inp.w_gate).astype(np.float64).T
+        u = x @ up(inp.w_up).astype(np.float64).T
+        assert np.allclose(r.g, g, rtol=0, atol=1e-12)
+        assert np.allclose(r.u, u, rtol=0, atol=1e-12)
+        ok = (np.abs(g) > 1e-9) & (np.abs(u) > 1e-9)
+        assert np.array_equal(((r.g > 0) & (r.u > 0))[ok], ((g > 0) & (u > 0))[ok])
+        # the active count equals the number of positive gate*up products with an open gate
+        assert r.n_active.tolist() == [int(((g[t] > 0) & (u[t] > 0)).sum()) for t in range(2)]
+
+
+def pin_ffn_skipzero_bitwise(lib=None):
+    """Summing only the active neurons, in ascending order, reproduces every bit
+    of the dense sum: the skipped terms are exact zeros."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 128, 640, gate_bias=-0.84, dtype=dtype, seed=8)
+        r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, lib=lib)
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        wd = up(inp.w_down_t).astype(np.float64)
+        for t in range(2):
+            y = np.zeros(128)
+            for i in r.active_set(t):
+                y += wd[i] * (r.g[t, i] * r.u[t, i])
+            assert np.array_equal(y.view(np.uint64), r.y[t].view(np.uint64))
+            assert 0 < len(r.active_set(t)) < 640
+
+
+def pin_moe_special_cases(lib=None):
+    # E = 1, k = 1: the MoE layer is exactly its single expert.
+    m = synth.make_moe(2, 64, 100, 1, 1, gate_bias=-0.5, dtype=synth.BF16, seed=9)
+    rm = oracle.moe(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, m.dtype, 1, lib=lib)
+    rf = oracle.ffn(m.x, m.w_gate[0], m.w_up[0], m.w_down_t[0], m.dtype, lib=lib)
+    assert np.array_equal(rm.y, rf.y)
+    assert np.all(rm.topk_w == 1.0)
+
+    # k = E: a full softmax mixture of all experts (numpy softmax and numpy sum).
+    E = 4
+    m = synth.make_moe(3, 32, 40, E, E, gate_bias=0.0, dtype=synth.F32, seed=10)
+    rm = oracle.moe(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, m.dtype, E, lib=lib)
+    x = m.x.astype(np.float64)
+    logits = x @ m.w_router.astype(np.float64).T
+    p = np.exp(logits - logits.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    y = np.zeros_like(x)
+    for e in range(E):
+        re = oracle.ffn(m.x, m.w_gate[e], m.w_up[e], m.w_down_t[e], m.dtype, lib=lib)
+        y += p[:, e:e + 1] * re.y
+    assert np.allclose(rm.y, y, rtol=1e-12, atol=1e-12 * np.abs(y).max())
+    assert np.allclose(np.sort(rm.topk_w, axis=1), np.sort(p, axis=1), rtol=1e-12, atol=0)
+
+    # top-2 of 8: the chosen experts are the two largest numpy logits, weights sum to 1.
+    m = synth.make_moe(6, 64, 32, 8, 2, gate_bias=-1.0, dtype=synth.BF16, seed=11)
+    rm = oracle.moe(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, m.dtype, 2, lib=lib)
+    logits = m.x.astype(np.float64) @ synth.bf16_bits_to_f32(m.w_router).astype(np.float64).T
+    for t in range(6):
+        order = np.argsort(-logits[t], kind="stable")
+        assert rm.topk_idx[t].tolist() == order[:2].tolist()
+        assert abs(rm.topk_w[t].sum() - 1.0) <= 4 * U
+        assert rm.topk_w[t, 0] >= rm.topk_w[t, 1]
+
+
+ALL_PINS = [pin_ffn_handworked, pin_moe_handworked, pin_ffn_bruteforce, pin_moe_bruteforce,
+            pin_ffn_zero_bias, pin_ffn_all_active_numpy, pin_ffn_sets_numpy, pin_ffn_skipzero_bitwise,
+            pin_moe_special_cases]
