@@ -1,0 +1,200 @@
+/*
+ * turbosparse.h — C ABI of the MI355X (gfx950) activation-sparse dReLU
+ * feed-forward library.
+ *
+ * The operation (Turbo Sparse, arXiv 2406.05955):
+ *   Eq. (gated-MLP), section 2, with F_act = ReLU applied to BOTH projections
+ *   (Eq. (drelu), section 3.2; no bias, section 3.2 footnote):
+ *       Combined(x) = max(0, x W_gate) * max(0, x W_up)
+ *       out(x)      = Combined(x) W_down
+ *   A neuron whose Combined activation is zero contributes nothing (sections
+ *   1 and 6.2), so the sparse entry points read a W_up row only for neurons
+ *   whose gate is positive, and a W_down row only for neurons whose Combined
+ *   activation is non-zero.  The result equals the dense definition exactly
+ *   up to floating-point summation order.
+ *   MoE form (section 6.2, "2 out of 8 experts"): a router picks top_k experts
+ *   per token and each routed expert is a dReLU FFN.  Router details, which
+ *   the paper leaves to Mixtral: logits = W_r x, p = softmax(logits), the
+ *   top_k largest p (lower expert index wins exact ties), weights
+ *   w = p / sum(p over the chosen experts), out = sum_k w_k FFN_{e_k}(x).
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller.  The
+ *     library allocates and frees nothing; scratch memory is the caller's
+ *     workspace `ws` of `ws_bytes` bytes (query the size first).
+ *   - Layout: x and out are fp32 row-major [batch][hidden].  Every weight
+ *     matrix is neuron-major [inter][hidden], row-major, in `wdtype`
+ *     (TS_F32: float, TS_BF16: bfloat16 bit patterns, 2 bytes).  Row i of
+ *     w_down_t is neuron i's output row, i.e. the paper's W_down row i.
+ *     MoE experts are packed [n_experts][inter][hidden]; the router is
+ *     [n_experts][hidden] in `wdtype`.
+ *   - Arithmetic: fp32 accumulation; x, the gate / up projections and
+ *     Combined stay fp32.  An active set is defined by strict comparisons
+ *     (gate > 0; Combined non-zero iff gate > 0 and up > 0).
+ *   - `out` is overwritten, never accumulated into.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL = the default stream); results are valid after the caller
+ *     synchronises that stream.  Concurrent calls need distinct workspaces.
+ *     Workspace contents after a call are unspecified.
+ *   - All argument checks run on the host before anything is enqueued.  On
+ *     any error the call returns a non-zero ts_status, enqueues nothing and
+ *     leaves every output untouched.  A failed kernel launch returns
+ *     TS_ERR_HIP (ts_last_error() has the HIP message).  Errors during
+ *     execution surface at the caller's stream synchronisation.
+ *   - Constraints: 1 <= batch <= 256; inter >= 1; hidden >= 8 and
+ *     hidden % 8 == 0 (TS_BF16) or hidden % 4 == 0 (TS_F32); hidden <= 8192
+ *     (TS_BF16) or <= 4096 (TS_F32); 1 <= n_experts <= 64;
+ *     1 <= top_k <= min(n_experts, 8); x, weights, out, topk_w, topk_idx
+ *     and ws 16-byte aligned; stats arrays 4-byte aligned.
+ *   - Non-finite inputs give unspecified (but memory-safe) results.
+ *   - No exceptions cross this interface.
+ */
+#ifndef TURBOSPARSE_H
+#define TURBOSPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TS_OK = 0,
+    TS_ERR_NULL = 1,        /* a required pointer is NULL */
+    TS_ERR_SHAPE = 2,       /* batch / hidden / inter / n_experts / top_k out of range */
+    TS_ERR_DTYPE = 3,       /* unknown ts_dtype */
+    TS_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+    TS_ERR_WORKSPACE = 5,   /* ws is NULL or ws_bytes is below the required size */
+    TS_ERR_HIP = 6,         /* a HIP runtime call or kernel launch failed */
+    TS_ERR_UNSUPPORTED = 7  /* valid request this build does not serve (e.g. stats on a dense call) */
+} ts_status;
+
+typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
+
+/*
+ * Optional per-token activity report (device pointers, each nullable).  For
+ * ts_ffn_sparse, "token" t indexes the batch; for ts_moe_sparse the report is
+ * per (token, routed slot) pair, index t * top_k + k, slot k in rank order.
+ *   n_gate[t]      |G_t|, G_t = {i : gate_{t,i} > 0}
+ *   n_active[t]    |A_t|, A_t = {i : gate_{t,i} > 0 and up_{t,i} > 0}
+ *   gate_idx[t*inter .. t*inter + n_gate[t])      G_t ascending
+ *   active_idx[t*inter .. t*inter + n_active[t])  A_t ascending
+ *   n_union[0..1]  |union_t G_t|, |union_t A_t| over the batch (ts_ffn_sparse
+ *                  only; these are the rows the batched path reads)
+ * Entries past a token's count are unspecified.  Producing the report costs
+ * extra small kernels; leave the pointer NULL on timed paths.
+ */
+typedef struct {
+    int32_t *n_gate;
+    int32_t *n_active;
+    int32_t *gate_idx;
+    int32_t *active_idx;
+    int32_t *n_union;
+} ts_ffn_stats;
+
+/* Workspace bytes needed by ts_ffn_sparse / ts_ffn_dense for these sizes
+ * (0 if the sizes are out of range). */
+size_t ts_ffn_workspace_bytes(int batch, int hidden, int inter, ts_dtype wdtype);
+
+/*
+ * Activation-sparse dReLU FFN: out[t] = sum_{i in A_t} Combined_{t,i} *
+ * w_down_t[i][:], with W_gate read whole and W_up / W_down rows read only for
+ * G_t / A_t (Eq. drelu; section 6.2's zero-activation skipping).
+ *   x [batch][hidden] fp32; w_gate, w_up, w_down_t [inter][hidden] wdtype;
+ *   out [batch][hidden] fp32; stats nullable; ws/ws_bytes workspace;
+ *   stream hipStream_t or NULL.
+ * batch == 1 uses the fused single-token kernels; batch > 1 reads every
+ * weight row at most once for the whole batch (rows of the union of the
+ * tokens' active sets) and runs the contraction on the matrix cores.
+ */
+ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                        ts_dtype wdtype, int batch, int hidden, int inter, float *out,
+                        const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Dense comparator: the same function (Eq. gated-MLP with dReLU) computed
+ * over every neuron, reading all three matrices in full.  Same arguments as
+ * ts_ffn_sparse without the stats report.
+ */
+ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                       ts_dtype wdtype, int batch, int hidden, int inter, float *out, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* Workspace bytes for ts_moe_sparse / ts_moe_dense (0 if out of range). */
+size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, int top_k,
+                              ts_dtype wdtype);
+
+/*
+ * Top-k MoE layer with activation-sparse dReLU experts (section 6.2).
+ *   x [batch][hidden] fp32; w_router [n_experts][hidden] wdtype;
+ *   w_gate, w_up, w_down_t [n_experts][inter][hidden] wdtype;
+ *   out [batch][hidden] fp32;
+ *   topk_idx [batch][top_k] int32 (nullable): chosen experts, rank order;
+ *   topk_w [batch][top_k] fp32 (nullable): their renormalised weights;
+ *   stats (nullable): per (token, slot) report, see ts_ffn_stats;
+ *   ws / ws_bytes / stream as above.
+ * The routing decision never leaves the device.
+ */
+ts_status ts_moe_sparse(const float *x, const void *w_router, const void *w_gate, const void *w_up,
+                        const void *w_down_t, ts_dtype wdtype, int batch, int hidden, int inter,
+                        int n_experts, int top_k, float *out, int32_t *topk_idx, float *topk_w,
+                        const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
+/* Dense comparator of ts_moe_sparse: same routing, every routed expert
+ * computed densely.  Same arguments without the stats report. */
+ts_status ts_moe_dense(const float *x, const void *w_router, const void *w_gate, const void *w_up,
+                       const void *w_down_t, ts_dtype wdtype, int batch, int hidden, int inter,
+                       int n_experts, int top_k, float *out, int32_t *topk_idx, float *topk_w,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* Human-readable name of a status code (static string). */
+const char *ts_status_str(ts_status s);
+
+/* Message of the last TS_ERR_HIP on the calling thread ("" if none). */
+const char *ts_last_error(void);
+
+/* Library version string (static). */
+const char *ts_version(void);
+
+/* ------------------------------------------------------------------------
+ * Measurement support (not part of the FFN operation).
+ */
+
+/*
+ * Per-kernel timing.  While enabled, every ts_* call records a HIP event
+ * pair around each kernel it launches, on the call's stream.  ts_prof_read
+ * synchronises on the recorded events and returns, for the kernel named
+ * `kernel` ("ffn_main", "ffn_reduce", "ffn_stats", "moe_router",
+ * "batch_gate", "batch_up", "batch_down", "batch_reduce", "probe_read",
+ * "probe_copy"), the number of launches and their summed duration in
+ * milliseconds since the last ts_prof_reset.  Returns TS_ERR_HIP on a
+ * HIP failure, TS_ERR_NULL for a NULL output pointer.  Not thread-safe.
+ */
+void ts_prof_enable(int on);
+void ts_prof_reset(void);
+ts_status ts_prof_read(const char *kernel, long *launches, double *total_ms);
+
+/*
+ * HBM probes.  ts_probe_read streams `bytes` (multiple of 16) from `src` and
+ * writes one float per workgroup into `sink` (at least 4096 floats); it
+ * measures the achievable read bandwidth.  ts_probe_copy copies `bytes`
+ * (multiple of 16) from src to dst; its HBM counter readings calibrate the
+ * traffic counters against a transfer of known size.
+ */
+ts_status ts_probe_read(const void *src, size_t bytes, float *sink, void *stream);
+ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
+
+/*
+ * Tuning knobs (process-wide; 0 restores the default).  Keys:
+ *   "ffn_tile"   neurons per workgroup of the single-token kernel (8..64,
+ *                multiple of 8)
+ * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
+ */
+ts_status ts_tune_set(const char *key, int value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TURBOSPARSE_H */

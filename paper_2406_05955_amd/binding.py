@@ -1,0 +1,235 @@
+"""Thin ctypes binding of libturbosparse.so (include/turbosparse.h).
+
+Argument marshalling only: torch tensors supply device memory and the
+stream; every step of the FFN runs in the library's HIP kernels.  There is no
+fallback: if the library is missing this module raises on import.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libturbosparse.so")
+
+TS_F32 = 0
+TS_BF16 = 1
+
+STATUS = {0: "TS_OK", 1: "TS_ERR_NULL", 2: "TS_ERR_SHAPE", 3: "TS_ERR_DTYPE", 4: "TS_ERR_ALIGN",
+          5: "TS_ERR_WORKSPACE", 6: "TS_ERR_HIP", 7: "TS_ERR_UNSUPPORTED"}
+
+EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_dense", "ts_moe_workspace_bytes", "ts_moe_sparse",
+            "ts_moe_dense", "ts_status_str", "ts_last_error", "ts_version", "ts_prof_enable", "ts_prof_reset",
+            "ts_prof_read", "ts_probe_read", "ts_probe_copy", "ts_tune_set"]
+
+
+class TSError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str = ""):
+        self.code = code
+        super().__init__(f"{where}: {STATUS.get(code, code)}" + (f" ({detail})" if detail else ""))
+
+
+class ffn_stats_t(ctypes.Structure):
+    _fields_ = [("n_gate", ctypes.c_void_p), ("n_active", ctypes.c_void_p), ("gate_idx", ctypes.c_void_p),
+                ("active_idx", ctypes.c_void_p), ("n_union", ctypes.c_void_p)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2406_05955_amd.build` "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    st = ctypes.c_int
+    lib.ts_ffn_workspace_bytes.argtypes = [i, i, i, i]
+    lib.ts_ffn_workspace_bytes.restype = sz
+    lib.ts_ffn_sparse.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp, sz, vp]
+    lib.ts_ffn_sparse.restype = st
+    lib.ts_ffn_dense.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, sz, vp]
+    lib.ts_ffn_dense.restype = st
+    lib.ts_moe_workspace_bytes.argtypes = [i, i, i, i, i, i]
+    lib.ts_moe_workspace_bytes.restype = sz
+    lib.ts_moe_sparse.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, vp, vp, sz, vp]
+    lib.ts_moe_sparse.restype = st
+    lib.ts_moe_dense.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, vp, sz, vp]
+    lib.ts_moe_dense.restype = st
+    lib.ts_status_str.argtypes = [st]
+    lib.ts_status_str.restype = ctypes.c_char_p
+    lib.ts_last_error.argtypes = []
+    lib.ts_last_error.restype = ctypes.c_char_p
+    lib.ts_version.argtypes = []
+    lib.ts_version.restype = ctypes.c_char_p
+    lib.ts_prof_enable.argtypes = [i]
+    lib.ts_prof_enable.restype = None
+    lib.ts_prof_reset.argtypes = []
+    lib.ts_prof_reset.restype = None
+    lib.ts_prof_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_long), ctypes.POINTER(ctypes.c_double)]
+    lib.ts_prof_read.restype = st
+    lib.ts_probe_read.argtypes = [vp, sz, vp, vp]
+    lib.ts_probe_read.restype = st
+    lib.ts_probe_copy.argtypes = [vp, vp, sz, vp]
+    lib.ts_probe_copy.restype = st
+    lib.ts_tune_set.argtypes = [ctypes.c_char_p, i]
+    lib.ts_tune_set.restype = st
+    return lib
+
+
+lib = _load()
+
+
+def _check(code: int, where: str):
+    if code != 0:
+        detail = lib.ts_last_error().decode() if code == 6 else ""
+        raise TSError(code, where, detail)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def wdtype_of(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return TS_F32
+    if t.dtype == torch.bfloat16:
+        return TS_BF16
+    raise TypeError(f"weights must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+def ffn_workspace_bytes(batch: int, hidden: int, inter: int, wdtype: int) -> int:
+    return int(lib.ts_ffn_workspace_bytes(batch, hidden, inter, wdtype))
+
+
+def moe_workspace_bytes(batch: int, hidden: int, inter: int, n_experts: int, top_k: int, wdtype: int) -> int:
+    return int(lib.ts_moe_workspace_bytes(batch, hidden, inter, n_experts, top_k, wdtype))
+
+
+def _workspace(nbytes: int, device, ws):
+    if ws is not None:
+        return ws
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _stats_struct(batch_slots: int, inter: int, device, want: bool):
+    if not want:
+        return None, None
+    d = {
+        "n_gate": torch.empty(batch_slots, dtype=torch.int32, device=device),
+        "n_active": torch.empty(batch_slots, dtype=torch.int32, device=device),
+        "gate_idx": torch.empty(batch_slots, inter, dtype=torch.int32, device=device),
+        "active_idx": torch.empty(batch_slots, inter, dtype=torch.int32, device=device),
+    }
+    s = ffn_stats_t(_ptr(d["n_gate"]), _ptr(d["n_active"]), _ptr(d["gate_idx"]), _ptr(d["active_idx"]), None)
+    return s, d
+
+
+def ffn_sparse(x, w_gate, w_up, w_down_t, out=None, stats: bool = False, union: bool = False, ws=None,
+               stream=None):
+    """ts_ffn_sparse.  x [B][H] f32; weights [I][H] f32/bf16.  Returns out, or
+    (out, stats dict) when stats/union is requested."""
+    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    B, H = x.shape
+    I = w_gate.shape[0]
+    dt = wdtype_of(w_gate)
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    ws = _workspace(ffn_workspace_bytes(B, H, I, dt), x.device, ws)
+    st, d = _stats_struct(B, I, x.device, stats or union)
+    if union:
+        d["n_union"] = torch.empty(2, dtype=torch.int32, device=x.device)
+        st.n_union = _ptr(d["n_union"])
+    code = lib.ts_ffn_sparse(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out),
+                             ctypes.byref(st) if st is not None else None, _ptr(ws), ws.numel(), _stream(stream))
+    _check(code, "ts_ffn_sparse")
+    return (out, d) if d is not None else out
+
+
+def ffn_dense(x, w_gate, w_up, w_down_t, out=None, ws=None, stream=None):
+    """ts_ffn_dense (all neurons, all three matrices read)."""
+    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    B, H = x.shape
+    I = w_gate.shape[0]
+    dt = wdtype_of(w_gate)
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    ws = _workspace(ffn_workspace_bytes(B, H, I, dt), x.device, ws)
+    code = lib.ts_ffn_dense(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out), _ptr(ws),
+                            ws.numel(), _stream(stream))
+    _check(code, "ts_ffn_dense")
+    return out
+
+
+def moe_sparse(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, stats: bool = False, ws=None,
+               stream=None, dense: bool = False):
+    """ts_moe_sparse (or ts_moe_dense with dense=True).  Returns
+    (out, topk_idx, topk_w) or (out, topk_idx, topk_w, stats dict)."""
+    _need_cuda(x, w_router, w_gate, w_up, w_down_t, out)
+    B, H = x.shape
+    E, I = w_gate.shape[0], w_gate.shape[1]
+    dt = wdtype_of(w_gate)
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    idx = torch.empty(B, top_k, dtype=torch.int32, device=x.device)
+    wts = torch.empty(B, top_k, dtype=torch.float32, device=x.device)
+    ws = _workspace(moe_workspace_bytes(B, H, I, E, top_k, dt), x.device, ws)
+    if dense:
+        code = lib.ts_moe_dense(_ptr(x), _ptr(w_router), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, E,
+                                top_k, _ptr(out), _ptr(idx), _ptr(wts), _ptr(ws), ws.numel(), _stream(stream))
+        _check(code, "ts_moe_dense")
+        return out, idx, wts
+    st, d = _stats_struct(B * top_k, I, x.device, stats)
+    code = lib.ts_moe_sparse(_ptr(x), _ptr(w_router), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, E,
+                             top_k, _ptr(out), _ptr(idx), _ptr(wts), ctypes.byref(st) if st is not None else None,
+                             _ptr(ws), ws.numel(), _stream(stream))
+    _check(code, "ts_moe_sparse")
+    return (out, idx, wts, d) if d is not None else (out, idx, wts)
+
+
+def moe_dense(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, ws=None, stream=None):
+    return moe_sparse(x, w_router, w_gate, w_up, w_down_t, top_k, out=out, ws=ws, stream=stream, dense=True)
+
+
+def probe_read(src: torch.Tensor, sink: torch.Tensor, stream=None):
+    _check(lib.ts_probe_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)),
+           "ts_probe_read")
+
+
+def probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
+    _check(lib.ts_probe_copy(_ptr(src), _ptr(dst), src.numel() * src.element_size(), _stream(stream)),
+           "ts_probe_copy")
+
+
+def prof_enable(on: bool):
+    lib.ts_prof_enable(1 if on else 0)
+
+
+def prof_reset():
+    lib.ts_prof_reset()
+
+
+def prof_read(kernel: str):
+    n = ctypes.c_long()
+    ms = ctypes.c_double()
+    _check(lib.ts_prof_read(kernel.encode(), ctypes.byref(n), ctypes.byref(ms)), "ts_prof_read")
+    return int(n.value), float(ms.value)
+
+
+def tune_set(key: str, value: int):
+    _check(lib.ts_tune_set(key.encode(), int(value)), "ts_tune_set")
+
+
+def version() -> str:
+    return lib.ts_version().decode()

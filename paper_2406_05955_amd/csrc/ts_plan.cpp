@@ -1,0 +1,164 @@
+// Host-side planning and validation (no HIP headers; see ts_plan.h).
+#include "ts_plan.h"
+
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+
+namespace ts {
+
+namespace {
+std::atomic<int> g_tile{0};
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
+}  // namespace
+
+int tuned_tile() { return g_tile.load(); }
+
+// Neurons per workgroup for the single-token kernel: enough workgroups to
+// give every compute unit one (256 on MI355X), rounded to a multiple of 8
+// rows, at most one wave-ballot (64) per tile.
+int choose_tile(int inter) {
+    int t = tuned_tile();
+    if (t > 0) return t;
+    int per = (inter + kTargetTiles - 1) / kTargetTiles;
+    per = (per + 7) / 8 * 8;
+    return std::min(kMaxTile, std::max(8, per));
+}
+
+ts_status check_dims(int batch, int hidden, int inter, ts_dtype dt) {
+    if (dt != TS_F32 && dt != TS_BF16) return TS_ERR_DTYPE;
+    if (batch < 1 || batch > kMaxBatch || inter < 1 || hidden < 8) return TS_ERR_SHAPE;
+    if (dt == TS_BF16 && (hidden % 8 != 0 || hidden > 8192)) return TS_ERR_SHAPE;
+    if (dt == TS_F32 && (hidden % 4 != 0 || hidden > 4096)) return TS_ERR_SHAPE;
+    // every [inter][hidden] matrix must be indexable with 64-bit offsets and
+    // the per-slot neuron count must fit a 32-bit index
+    if ((long long)inter * (long long)hidden > (1LL << 40)) return TS_ERR_SHAPE;
+    return TS_OK;
+}
+
+ts_status check_moe_dims(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt) {
+    ts_status s = check_dims(batch, hidden, inter, dt);
+    if (s != TS_OK) return s;
+    if (n_experts < 1 || n_experts > kMaxExperts) return TS_ERR_SHAPE;
+    if (top_k < 1 || top_k > n_experts || top_k > kMaxTopK) return TS_ERR_SHAPE;
+    return TS_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+ts_status check_stats(const ts_ffn_stats *s) {
+    if (!s) return TS_OK;
+    const void *ps[] = {s->n_gate, s->n_active, s->gate_idx, s->active_idx, s->n_union};
+    for (const void *p : ps)
+        if (p && !aligned4(p)) return TS_ERR_ALIGN;
+    return TS_OK;
+}
+
+bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p) {
+    if (check_dims(1, hidden, inter, dt) != TS_OK || slots < 1 || slots_per_out < 1 ||
+        slots % slots_per_out != 0)
+        return false;
+    SlotPlan q;
+    q.hidden = hidden;
+    q.inter = inter;
+    q.esz = esize(dt);
+    q.ce = 16 / q.esz;
+    q.nch = hidden / q.ce;
+    int need = (q.nch + 63) / 64;
+    q.nc = 1;
+    while (q.nc < need) q.nc <<= 1;
+    q.tile = choose_tile(inter);
+    q.ntiles = (inter + q.tile - 1) / q.tile;
+    q.slots = slots;
+    q.slots_per_out = slots_per_out;
+    q.outs = slots / slots_per_out;
+    size_t nst = (size_t)slots * (size_t)q.ntiles;
+    size_t off = 0;
+    q.off_cnt = off;
+    off = align256(off + nst * 2 * sizeof(int32_t));
+    q.off_gseg = off;
+    off = align256(off + nst * (size_t)q.tile * sizeof(int32_t));
+    q.off_aseg = off;
+    off = align256(off + nst * (size_t)q.tile * sizeof(int32_t));
+    q.off_partial = off;
+    off = align256(off + nst * (size_t)hidden * sizeof(float));
+    q.off_route_idx = off;
+    off = align256(off + (size_t)slots * sizeof(int32_t));
+    q.off_route_w = off;
+    off = align256(off + (size_t)slots * sizeof(float));
+    q.off_aux = off;  // union flags of the activity report: [2][inter]
+    off = align256(off + (size_t)2 * (size_t)inter * sizeof(int32_t));
+    q.total = off;
+    *p = q;
+    return true;
+}
+
+bool plan_batch(int batch, int hidden, int inter, ts_dtype dt, BatchPlan *p) {
+    if (check_dims(batch, hidden, inter, dt) != TS_OK) return false;
+    BatchPlan q;
+    q.batch = batch;
+    q.hidden = hidden;
+    q.inter = inter;
+    q.esz = esize(dt);
+    q.bpad = batch <= 16 ? 16 : 32 * ((batch + 31) / 32);
+    q.total = 0;
+    *p = q;
+    return true;
+}
+
+size_t ffn_ws_bytes(int batch, int hidden, int inter, ts_dtype dt) {
+    if (check_dims(batch, hidden, inter, dt) != TS_OK) return 0;
+    SlotPlan sp;
+    if (!plan_slots(hidden, inter, dt, batch, 1, &sp)) return 0;
+    return sp.total;
+}
+
+size_t moe_ws_bytes(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt) {
+    if (check_moe_dims(batch, hidden, inter, n_experts, top_k, dt) != TS_OK) return 0;
+    SlotPlan sp;
+    if (!plan_slots(hidden, inter, dt, batch * top_k, top_k, &sp)) return 0;
+    return sp.total;
+}
+
+}  // namespace ts
+
+extern "C" {
+
+const char *ts_status_str(ts_status s) {
+    switch (s) {
+    case TS_OK: return "TS_OK";
+    case TS_ERR_NULL: return "TS_ERR_NULL: a required pointer is NULL";
+    case TS_ERR_SHAPE: return "TS_ERR_SHAPE: size argument out of range";
+    case TS_ERR_DTYPE: return "TS_ERR_DTYPE: unknown weight dtype";
+    case TS_ERR_ALIGN: return "TS_ERR_ALIGN: pointer not aligned";
+    case TS_ERR_WORKSPACE: return "TS_ERR_WORKSPACE: workspace missing or too small";
+    case TS_ERR_HIP: return "TS_ERR_HIP: HIP runtime failure";
+    case TS_ERR_UNSUPPORTED: return "TS_ERR_UNSUPPORTED: request not served by this build";
+    }
+    return "unknown ts_status";
+}
+
+size_t ts_ffn_workspace_bytes(int batch, int hidden, int inter, ts_dtype wdtype) {
+    return ts::ffn_ws_bytes(batch, hidden, inter, wdtype);
+}
+
+size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype wdtype) {
+    return ts::moe_ws_bytes(batch, hidden, inter, n_experts, top_k, wdtype);
+}
+
+ts_status ts_tune_set(const char *key, int value) {
+    if (!key) return TS_ERR_NULL;
+    if (std::strcmp(key, "ffn_tile") == 0) {
+        if (value != 0 && (value < 8 || value > ts::kMaxTile || value % 8 != 0)) return TS_ERR_SHAPE;
+        ts::g_tile.store(value);
+        return TS_OK;
+    }
+    return TS_ERR_SHAPE;
+}
+
+const char *ts_version(void) { return "turbosparse-gfx950 0.1"; }
+
+}  // extern "C"

@@ -1,0 +1,165 @@
+"""Parity of the HIP sparse dReLU FFN (ts_ffn_sparse / ts_ffn_dense, called
+through the C ABI) against the fp64 oracle on seeded inputs.
+
+Tolerances (from the workload definition): relative L2 error of the output
+<= 1e-5 with fp32 weights and <= 1e-2 with bf16 weights (fp32 accumulation
+in both).  Active sets: with fp32 weights, G and A must match the oracle
+exactly on every neuron with |gate| >= 1e-6 (and |up| >= 1e-6 for A); with
+bf16 weights the kernel still reads the exact bf16 values the oracle uses,
+so the only difference is fp32 vs fp64 rounding of a 4096-term dot product
+(|error| well under 1e-4): the sets must match exactly outside |gate|, |up|
+< 1e-4."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DEV, compare_sets, ffn_inputs_to_dev, list_of, rel_l2, to_dev
+from paper_2406_05955_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ts = pytest.importorskip("paper_2406_05955_amd.binding") if torch.cuda.is_available() else None
+
+
+def tol_for(dtype):
+    return 1e-5 if dtype == synth.F32 else 1e-2
+
+
+def set_thresh(dtype):
+    return 1e-6 if dtype == synth.F32 else 1e-4
+
+
+def check_ffn(inp, ref=None, sets=True):
+    B, H, I = inp.shape
+    ref = ref or oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out, st = ts.ffn_sparse(x, wg, wu, wd, stats=True)
+    torch.cuda.synchronize()
+    err = rel_l2(out.cpu().numpy(), ref.y)
+    assert err <= tol_for(inp.dtype), (B, H, I, err)
+    thr = set_thresh(inp.dtype)
+    for t in range(B):
+        g, u = ref.g[t], ref.u[t]
+        keep_g = np.abs(g) >= thr
+        keep_a = keep_g & (np.abs(u) >= thr)
+        assert compare_sets(list_of(st, "gate_idx", t, "n_gate"), g > 0, keep_g) == 0
+        assert compare_sets(list_of(st, "active_idx", t, "n_active"), (g > 0) & (u > 0), keep_a) == 0
+        if sets and np.all(keep_a | ~((g > 0) & (u > 0))) and np.all(keep_g | ~(g > 0)):
+            assert int(st["n_gate"][t]) == int(ref.n_gate[t])
+            assert int(st["n_active"][t]) == int(ref.n_active[t])
+    return out, st, ref
+
+
+def test_config0_fp32_full():
+    """H=512, I=1792, fp32, gate bias -0.84, seed 0: every output and both sets."""
+    inp = synth.make_ffn(1, 512, 1792, gate_bias=-0.84, dtype=synth.F32, seed=0)
+    out, st, ref = check_ffn(inp)
+    assert int(st["n_gate"][0]) == int(ref.n_gate[0])
+    assert int(st["n_active"][0]) == int(ref.n_active[0])
+    assert 250 < int(ref.n_gate[0]) < 470 and 100 < int(ref.n_active[0]) < 260
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("B,H,I", [(1, 8, 1), (1, 8, 7), (1, 40, 65), (3, 200, 130), (1, 1000, 777),
+                                   (2, 512, 4096), (1, 2048, 3001), (1, 4096, 2000)])
+def test_ragged_shapes(dtype, B, H, I):
+    if dtype == synth.BF16 and H % 8:
+        H += 8 - H % 8
+    inp = synth.make_ffn(B, H, I, gate_bias=-0.5, dtype=dtype, seed=[B, H, I])
+    check_ffn(inp)
+
+
+@pytest.mark.parametrize("tile", [8, 16, 40, 64])
+def test_tile_sizes(tile):
+    ts.tune_set("ffn_tile", tile)
+    try:
+        inp = synth.make_ffn(2, 1024, 1500, gate_bias=-0.84, dtype=synth.BF16, seed=tile)
+        check_ffn(inp)
+    finally:
+        ts.tune_set("ffn_tile", 0)
+
+
+def test_bf16_h8192():
+    inp = synth.make_ffn(1, 8192, 600, gate_bias=-0.84, dtype=synth.BF16, seed=3)
+    check_ffn(inp)
+
+
+def test_degenerate_all_closed_and_all_open():
+    closed = synth.make_ffn(2, 256, 700, gate_bias=-100.0, dtype=synth.F32, seed=4)
+    out, st, ref = check_ffn(closed)
+    assert torch.all(out == 0).item()
+    assert st["n_gate"].cpu().tolist() == [0, 0] and st["n_active"].cpu().tolist() == [0, 0]
+    opened = synth.make_ffn(1, 256, 700, gate_bias=100.0, dtype=synth.F32, seed=5)
+    opened.w_up[:, 0] = 100.0
+    out, st, ref = check_ffn(opened)
+    assert st["n_active"].cpu().tolist() == [700]
+
+
+def test_mistral_shape_layer_full():
+    """H=4096, I=14336, bf16, 90% Combined sparsity (b=-0.8416), drawn on the
+    device exactly as the benchmark draws its layers; every output compared."""
+    L = synth.make_ffn_stack_torch(2, 1, 4096, 14336, gate_bias=-0.8416, dtype=synth.BF16, seed=0, device=DEV)
+    for l in range(2):
+        x, wg, wu, wd = L["x"][l], L["w_gate"][l], L["w_up"][l], L["w_down_t"][l]
+        inp = synth.FFNInputs(x=x.cpu().numpy(), w_gate=synth.tensor_to_host_array(wg, synth.BF16),
+                              w_up=synth.tensor_to_host_array(wu, synth.BF16),
+                              w_down_t=synth.tensor_to_host_array(wd, synth.BF16), dtype=synth.BF16,
+                              gate_bias=-0.8416)
+        out, st, ref = check_ffn(inp)
+        frac = 1.0 - float(ref.n_active[0]) / 14336
+        assert 0.87 < frac < 0.93, frac
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_dense_comparator(dtype):
+    inp = synth.make_ffn(2, 1024, 3000, gate_bias=-0.84, dtype=dtype, seed=6)
+    ref = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out_d = ts.ffn_dense(x, wg, wu, wd)
+    out_s = ts.ffn_sparse(x, wg, wu, wd)
+    torch.cuda.synchronize()
+    assert rel_l2(out_d.cpu().numpy(), ref.y) <= tol_for(dtype)
+    assert rel_l2(out_d.cpu().numpy(), out_s.cpu().numpy().astype(np.float64)) <= tol_for(dtype)
+
+
+def test_deterministic_and_workspace_canaries():
+    """Two calls give the same bits, also when the workspace starts full of
+    NaNs (a read of a partial row that was never written would show)."""
+    inp = synth.make_ffn(1, 4096, 14336 // 4, gate_bias=-1.2816, dtype=synth.BF16, seed=7)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    nbytes = ts.ffn_workspace_bytes(1, 4096, 14336 // 4, 1)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    ws.view(torch.float32)[: nbytes // 4].fill_(float("nan"))
+    a = ts.ffn_sparse(x, wg, wu, wd, ws=ws)
+    b = ts.ffn_sparse(x, wg, wu, wd)
+    ws.view(torch.float32)[: nbytes // 4].fill_(float("nan"))
+    c = ts.ffn_sparse(x, wg, wu, wd, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(a).all().item()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    assert torch.equal(a.view(torch.int32), c.view(torch.int32))
+
+
+def test_batch_union_counts():
+    inp = synth.make_ffn(8, 1024, 2048, gate_bias=-0.84, dtype=synth.BF16, seed=8)
+    ref = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out, st = ts.ffn_sparse(x, wg, wu, wd, union=True)
+    torch.cuda.synchronize()
+    assert rel_l2(out.cpu().numpy(), ref.y) <= 1e-2
+    ug = int((ref.g > 0).any(axis=0).sum())
+    ua = int(((ref.g > 0) & (ref.u > 0)).any(axis=0).sum())
+    got = st["n_union"].cpu().tolist()
+    assert abs(got[0] - ug) <= 2 and abs(got[1] - ua) <= 2, (got, ug, ua)
+
+
+def test_error_leaves_output_untouched():
+    inp = synth.make_ffn(1, 512, 100, dtype=synth.F32, seed=9)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out = torch.full((1, 512), 7.0, device=DEV)
+    small = torch.empty(16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(ts.TSError):
+        ts.ffn_sparse(x, wg, wu, wd, out=out, ws=small)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0).item()

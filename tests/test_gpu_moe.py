@@ -1,0 +1,84 @@
+"""Parity of the HIP top-k MoE layer (ts_moe_sparse / ts_moe_dense through
+the C ABI) against the fp64 oracle.  Routing is compared exactly except for
+tokens whose k-th and (k+1)-th oracle probabilities are within 1e-6
+(relative) of each other; outputs to relative L2 <= 1e-5 (fp32 weights) /
+1e-2 (bf16 weights)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DEV, compare_sets, rel_l2, to_dev
+from paper_2406_05955_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ts = pytest.importorskip("paper_2406_05955_amd.binding") if torch.cuda.is_available() else None
+
+
+def near_tie(probs_t, K):
+    p = np.sort(probs_t)[::-1]
+    return K < p.size and abs(p[K - 1] - p[K]) <= 1e-6 * p[K - 1]
+
+
+def run_moe(m, stats=False, dense=False):
+    args = [to_dev(m.x), to_dev(m.w_router), to_dev(m.w_gate), to_dev(m.w_up), to_dev(m.w_down_t)]
+    if dense:
+        return ts.moe_dense(*args, m.top_k)
+    return ts.moe_sparse(*args, m.top_k, stats=stats)
+
+
+def check_moe(m, dense=False):
+    B, H, I, E, K = m.shape
+    ref = oracle.moe(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, m.dtype, K)
+    res = run_moe(m, stats=not dense, dense=dense)
+    torch.cuda.synchronize()
+    out, idx, w = res[0], res[1].cpu().numpy(), res[2].cpu().numpy()
+    ties = [near_tie(ref.probs[t], K) for t in range(B)]
+    for t in range(B):
+        if ties[t]:
+            continue
+        assert idx[t].tolist() == ref.topk_idx[t].tolist(), (t, idx[t], ref.topk_idx[t])
+        assert np.allclose(w[t], ref.topk_w[t], rtol=1e-5, atol=1e-6)
+    keep = [t for t in range(B) if not ties[t]]
+    tol = 1e-5 if m.dtype == synth.F32 else 1e-2
+    assert rel_l2(out.cpu().numpy()[keep], ref.y[keep]) <= tol
+    if not dense:
+        st = res[3]
+        thr = 1e-6 if m.dtype == synth.F32 else 1e-4
+        for t in keep:
+            for k in range(K):
+                s = t * K + k
+                g, u = ref.g[t, k], ref.u[t, k]
+                keep_a = (np.abs(g) >= thr) & (np.abs(u) >= thr)
+                n = int(st["n_active"][s])
+                got = st["active_idx"][s, :n].cpu().numpy()
+                assert compare_sets(got, (g > 0) & (u > 0), keep_a) == 0
+    return ref, res
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("B,H,I,E,K", [(1, 512, 1024, 8, 2), (16, 512, 700, 8, 2), (3, 256, 130, 4, 4),
+                                       (2, 1024, 333, 1, 1), (5, 640, 256, 64, 8), (1, 4096, 2048, 8, 2)])
+def test_moe_shapes(dtype, B, H, I, E, K):
+    m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=dtype, seed=[B, H, I, E, K])
+    check_moe(m)
+
+
+def test_moe_dense_matches():
+    m = synth.make_moe(4, 512, 900, 8, 2, gate_bias=-0.5244, dtype=synth.BF16, seed=12)
+    check_moe(m, dense=True)
+
+
+def test_moe_mixtral_shape_b1():
+    """E=8, H=4096, I=14336 per expert, bf16, 97% in-expert sparsity, drawn
+    on the device like the benchmark's MoE layers."""
+    L = synth.make_moe_stack_torch(1, 1, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=0,
+                                   device=DEV)
+    h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
+    m = synth.MoEInputs(x=L["x"][0].cpu().numpy(), w_router=h(L["w_router"][0]), w_gate=h(L["w_gate"][0]),
+                        w_up=h(L["w_up"][0]), w_down_t=h(L["w_down_t"][0]), dtype=synth.BF16, top_k=2,
+                        gate_bias=-1.5548)
+    ref, res = check_moe(m)
+    n_act = res[3]["n_active"].cpu().numpy()
+    assert np.all(n_act < 0.06 * 14336)
