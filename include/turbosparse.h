@@ -187,8 +187,14 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
 
 /*
  * Tuning knobs (process-wide; 0 restores the default).  Keys:
- *   "ffn_tile"   neurons per workgroup of the single-token kernel (8..64,
- *                multiple of 8)
+ *   "ffn_tile"   neurons per workgroup of the fused single-token kernel
+ *                (4..64, multiple of 4)
+ *   "ffn_path"   0 = fused single-token kernel, 1 = split gate+up / down
+ *   "gate_tile"  neurons per workgroup of the split path's gate+up kernel
+ *                (4..64, multiple of 4)
+ *   "down_chunks" tile groups per slot in the split path's down kernel
+ *   "rif"        weight rows in flight per wave in the row dot products
+ *                (1 or 2)
  * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
  */
 ts_status ts_tune_set(const char *key, int value);

@@ -58,12 +58,48 @@ __device__ __forceinline__ void unpack<uint16_t>(const u32x4 v, float *f) {
     f[7] = __uint_as_float(v.w & 0xffff0000u);
 }
 
-// Butterfly sum over the 64 lanes of a wave.  Every lane ends with the same
-// bits: at each step both partners add the same two values.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float readlane_f32(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Sum over the 64 lanes of a wave with DPP moves inside each 16-lane row
+// (quad swaps, then rotations by 4 and 8) and the four row sums read into
+// scalars and added in a fixed order.  The result is wave-uniform and the
+// same bits on every run.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-    return v;
+    v += dpp_f32<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_f32<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp_f32<0x124>(v);  // row_ror:4
+    v += dpp_f32<0x128>(v);  // row_ror:8
+    return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
+}
+
+// 16-byte chunk c of a row, or zeros when c is out of range, without a
+// branch: the address is clamped to a valid chunk and the value masked, so a
+// run of such loads issues back to back.
+__device__ __forceinline__ u32x4 ld_stream_masked(const void *row, int c, int nch, int bytes_per_chunk, bool ok) {
+    const int cc = c < nch ? c : nch - 1;
+    u32x4 v = ld_stream(static_cast<const char *>(row) + (size_t)cc * bytes_per_chunk);
+    const bool keep = ok && c < nch;
+    return keep ? v : u32x4{0u, 0u, 0u, 0u};
+}
+
+// Same without the mask: chunks past the row end re-read its last chunk.
+// Callers pair such chunks with zero x values, so they add nothing.
+__device__ __forceinline__ u32x4 ld_stream_clamped(const void *row, int c, int nch) {
+    const int cc = c < nch ? c : nch - 1;
+    return ld_stream(static_cast<const char *>(row) + (size_t)cc * 16);
+}
+
+__device__ __forceinline__ f32x4 ld_f32x4_masked(const float *p, int i4, int n4) {
+    const int ii = i4 < n4 ? i4 : n4 - 1;
+    f32x4 v = *reinterpret_cast<const f32x4 *>(p + (size_t)ii * 4);
+    return i4 < n4 ? v : f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
 __device__ __forceinline__ int lane_prefix(uint64_t mask, int lane) {

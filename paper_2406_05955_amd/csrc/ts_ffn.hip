@@ -2,26 +2,32 @@
 // and the ts_ffn_* / ts_moe_* entry points.
 //
 // One slot is one token evaluated against one weight set (the FFN's, or the
-// routed expert's in the MoE layer).  For each slot the work is split into
-// tiles of `tile` consecutive neurons, one 512-thread workgroup (8 wave64s)
-// per tile, and each workgroup runs the whole dReLU FFN for its neurons:
+// routed expert's in the MoE layer).  Eq. (drelu) of Turbo Sparse (arXiv
+// 2406.05955): Combined = max(0, x W_gate) * max(0, x W_up), out = Combined
+// W_down.  Skipping the zero Combined terms (section 6.2) leaves the output
+// unchanged, so only the W_up rows of open gates and the W_down rows of
+// non-zero Combined activations are read.
 //
+// Two kernel sequences serve a call (both end in ffn_reduce, which sums
+// fp32 partial rows in a fixed order: deterministic, no atomics):
+//
+// fused  (ffn_fused, 8 waves per workgroup, one tile of neurons each)
 //   gate   every lane holds its share of x in registers; each wave dots whole
-//          W_gate rows (16-byte streaming loads, two rows in flight) and the
-//          results meet in LDS; one wave ballots `gate > 0` and prefix-counts
-//          the ballot into the tile's ascending open-gate list G.
-//   up     the waves dot the W_up rows of G only, Combined = gate * up where
-//          up > 0; a second ballot compacts the non-zero ones into A.
+//          W_gate rows (16-byte streaming loads, RIF rows in flight); the
+//          gates meet in LDS, one wave ballots `gate > 0` and prefix-counts
+//          the ballot into the tile's ascending open-gate list G;
+//   up     the waves dot the W_up rows of G; a second ballot compacts the
+//          neurons with up > 0 into A with Combined = gate * up;
 //   down   the 512 threads split the hidden dimension (16 bytes each) and run
-//          an axpy over the W_down_t rows of A in ascending order; the tile's
-//          partial output row goes to the workspace (skipped when A is empty).
+//          an axpy over the W_down_t rows of A in ascending order into the
+//          tile's partial output row.
+//   The dense comparator is this kernel with every neuron taken.
 //
-// A second kernel sums the partial rows of every tile in a fixed order
-// (deterministic, no atomics), applying the routing weights in the MoE form.
-//
-// Eq. (drelu) of Turbo Sparse (arXiv 2406.05955): Combined = max(0, x W_gate)
-// * max(0, x W_up); skipping the zero Combined terms (section 6.2) leaves
-// the output unchanged.
+// split  (ffn_gate_up with 4-wave workgroups, then ffn_down)
+//   gate and up as above, the tile's A segment and Combined values go to the
+//   workspace; ffn_down gives each (chunk of tiles, 64-chunk column slice) a
+//   workgroup that lists the chunk's active rows in LDS and accumulates
+//   their W_down_t slices into a partial row per chunk.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -32,6 +38,58 @@
 #include "turbosparse.h"
 
 namespace ts {
+
+constexpr int kDownUnroll = 8;
+
+// Lane `lane` keeps chunks lane, lane + 64, ... of x (fp32) in registers.
+template <typename WT, int NC>
+__device__ __forceinline__ void load_x(const float *__restrict__ x, int lane, int nch,
+                                       float (&xr)[NC][WTraits<WT>::CE]) {
+    constexpr int CE = WTraits<WT>::CE;
+    constexpr int Q = CE / 4;  // float4 per chunk
+    f32x4 v[NC][Q];
+#pragma unroll
+    for (int k = 0; k < NC; ++k)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) v[k][q] = ld_f32x4_masked(x, (lane + 64 * k) * Q + q, nch * Q);
+#pragma unroll
+    for (int k = 0; k < NC; ++k)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            xr[k][4 * q] = v[k][q].x;
+            xr[k][4 * q + 1] = v[k][q].y;
+            xr[k][4 * q + 2] = v[k][q].z;
+            xr[k][4 * q + 3] = v[k][q].w;
+        }
+}
+
+// Dot products of R weight rows with the x chunks held in registers.  All
+// R * NC loads are issued before any arithmetic; rows with valid[k] false
+// (and chunks past the row end) read a clamped address and count as zero.
+// Returns wave-uniform sums.
+template <typename WT, int NC, int R>
+__device__ __forceinline__ void dot_rows(const WT *const (&rows)[R], const bool (&valid)[R],
+                                         const float (&xr)[NC][WTraits<WT>::CE], int lane, int nch,
+                                         float (&out)[R]) {
+    constexpr int CE = WTraits<WT>::CE;
+    u32x4 v[R][NC];
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) v[k][c0] = ld_stream_masked(rows[k], lane + 64 * c0, nch, 16, valid[k]);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        float d = 0.f;
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) {
+            float f[CE];
+            unpack<WT>(v[k][c0], f);
+#pragma unroll
+            for (int e = 0; e < CE; ++e) d = fmaf(f[e], xr[c0][e], d);
+        }
+        out[k] = wave_sum(d);
+    }
+}
 
 struct SlotArgs {
     const float *x;          // [tokens][H]
@@ -48,43 +106,10 @@ struct SlotArgs {
     int want_seg;
 };
 
-constexpr int kDownUnroll = 8;
-
-// Dot products of R weight rows (those with valid[k]) with the x chunks held
-// in registers; all R rows' loads are issued before any arithmetic.  Every
-// lane returns the full sums.
-template <typename WT, int NC, int R>
-__device__ __forceinline__ void dot_rows(const WT *const (&rows)[R], const bool (&valid)[R],
-                                         const float (&xr)[NC][WTraits<WT>::CE], int lane, int nch,
-                                         float (&out)[R]) {
-    constexpr int CE = WTraits<WT>::CE;
-    u32x4 v[R][NC];
-#pragma unroll
-    for (int k = 0; k < R; ++k)
-#pragma unroll
-        for (int c0 = 0; c0 < NC; ++c0) {
-            const int c = lane + 64 * c0;
-            v[k][c0] = (valid[k] && c < nch) ? ld_stream(rows[k] + c * CE) : u32x4{0u, 0u, 0u, 0u};
-        }
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-        float d = 0.f;
-#pragma unroll
-        for (int c0 = 0; c0 < NC; ++c0) {
-            float f[CE];
-            unpack<WT>(v[k][c0], f);
-#pragma unroll
-            for (int e = 0; e < CE; ++e) d = fmaf(f[e], xr[c0][e], d);
-        }
-        out[k] = wave_sum(d);
-    }
-}
-
-template <typename WT, int NC, bool DENSE>
-__global__ __launch_bounds__(kThreads) void ffn_slot_main(SlotArgs a) {
+template <typename WT, int NC, bool DENSE, int RIF>
+__global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
     constexpr int CE = WTraits<WT>::CE;
     constexpr int NCD = (NC * 64 + kThreads - 1) / kThreads;
-    constexpr int RIF = NC >= 16 ? 1 : 2;  // weight rows in flight per wave
 
     __shared__ float s_g[kMaxTile];
     __shared__ float s_h[kMaxTile];
@@ -110,23 +135,9 @@ __global__ __launch_bounds__(kThreads) void ffn_slot_main(SlotArgs a) {
     const WT *wg = reinterpret_cast<const WT *>(a.wg) + eoff + (size_t)n0 * H;
     const WT *wu = reinterpret_cast<const WT *>(a.wu) + eoff + (size_t)n0 * H;
     const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff + (size_t)n0 * H;
-    const float *x = a.x + (size_t)tok * H;
 
-    // x in registers: lane owns chunks lane, lane + 64, ... of every row.
     float xr[NC][CE];
-#pragma unroll
-    for (int k = 0; k < NC; ++k) {
-        const int c = lane + 64 * k;
-#pragma unroll
-        for (int e = 0; e < CE; e += 4) {
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if (c < nch) v = *reinterpret_cast<const f32x4 *>(x + c * CE + e);
-            xr[k][e] = v.x;
-            xr[k][e + 1] = v.y;
-            xr[k][e + 2] = v.z;
-            xr[k][e + 3] = v.w;
-        }
-    }
+    load_x<WT, NC>(a.x + (size_t)tok * H, lane, nch, xr);
 
     // ---- gate: wave w dots rows w, w+8, ..., RIF rows in flight ------------
     for (int r = wave; r < nt; r += RIF * kWaves) {
@@ -212,41 +223,35 @@ __global__ __launch_bounds__(kThreads) void ffn_slot_main(SlotArgs a) {
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
             const int aa = a0 + u;
-            const WT *row = wd + (size_t)(aa < na ? s_al[aa] : 0) * H;
+            const WT *row = wd + (size_t)s_al[aa < na ? aa : a0] * H;
 #pragma unroll
-            for (int kd = 0; kd < NCD; ++kd) {
-                const int c = tid + kThreads * kd;
-                v[u][kd] = (aa < na && c < nch) ? ld_stream(row + c * CE) : u32x4{0u, 0u, 0u, 0u};
-            }
+            for (int kd = 0; kd < NCD; ++kd)
+                v[u][kd] = ld_stream_masked(row, tid + kThreads * kd, nch, 16, aa < na);
         }
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
-            const int aa = a0 + u;
-            if (aa < na) {
-                const float hv = s_av[aa];
+            const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
 #pragma unroll
-                for (int kd = 0; kd < NCD; ++kd) {
-                    float f[CE];
-                    unpack<WT>(v[u][kd], f);
+            for (int kd = 0; kd < NCD; ++kd) {
+                float f[CE];
+                unpack<WT>(v[u][kd], f);
 #pragma unroll
-                    for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
-                }
+                for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
             }
         }
     }
 
+    // partial row (written for every tile; zeros when A is empty)
     const size_t pr = (size_t)slot * a.ntiles + tile;
-    if (na > 0) {
-        float *prow = a.partial + pr * H;
+    float *prow = a.partial + pr * H;
 #pragma unroll
-        for (int kd = 0; kd < NCD; ++kd) {
-            const int c = tid + kThreads * kd;
-            if (c < nch) {
+    for (int kd = 0; kd < NCD; ++kd) {
+        const int c = tid + kThreads * kd;
+        if (c < nch) {
 #pragma unroll
-                for (int e = 0; e < CE; e += 4)
-                    *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
-                        f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
-            }
+            for (int e = 0; e < CE; e += 4)
+                *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
+                    f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
         }
     }
     if (tid == 0) {
@@ -259,49 +264,464 @@ __global__ __launch_bounds__(kThreads) void ffn_slot_main(SlotArgs a) {
     }
 }
 
-// out[o][:] = sum over the slots s of output row o, and over tiles p in
-// ascending order, of w_s * partial[s][p][:] (w_s = 1 without routing).
-// Block: 32 columns (8 float4) x 32 row groups; grid (column blocks, outs).
-constexpr int kRedCols4 = 8;
-constexpr int kRedGroups = 32;
+// ---------------------------------------------------------------------------
+// Pipelined single-token kernel (the default sparse path).  Same work and
+// output per tile as ffn_fused, but each wave streams its own gate rows
+// (rows w, w+8, ... of the tile) two deep and, as soon as a row's gate is
+// known to be open, issues that row's W_up loads; the up dot is finished one
+// row later, while the wave's next gate rows are in flight.  The up traffic
+// therefore travels with the gate stream instead of forming a burst after
+// it, and no barrier separates the two.  Then, behind one barrier, wave 0
+// ballots the open gates and the non-zero Combined activations of the tile
+// and the 512 threads run the down axpy (hidden split over threads).
 
-__global__ __launch_bounds__(256) void ffn_reduce(const float *__restrict__ partial, const int32_t *__restrict__ cnt,
-                                                  int ntiles, int H, int slots_per_out,
-                                                  const float *__restrict__ slot_w, float *__restrict__ out) {
+template <typename WT, int NC>
+struct PipeWave {
+    static constexpr int CE = WTraits<WT>::CE;
+    const WT *wg, *wu;
+    const void *dummy;  // x: an L2-resident row-sized buffer for unused load slots
+    int H, nch, lane;
+    float (&xr)[NC][CE];
+    float *s_g, *s_h;
+    int *s_on;
+
+    // Loads are unconditional (an unused slot reads `dummy`), so no branch
+    // separates a load from its consumer and all of a wave's loads stay in
+    // flight across steps.  Chunks past the row end meet zero x values.
+    __device__ void issue(const void *row, u32x4 (&v)[NC]) {
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) v[c0] = ld_stream_clamped(row, lane + 64 * c0, nch);
+    }
+    __device__ float dot(const u32x4 (&v)[NC]) {
+        float d = 0.f;
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) {
+            float f[CE];
+            unpack<WT>(v[c0], f);
+#pragma unroll
+            for (int e = 0; e < CE; ++e) d = fmaf(f[e], xr[c0][e], d);
+        }
+        return wave_sum(d);
+    }
+    // One row: gate dot from gcur; issue the row's up loads into ucur (its
+    // W_up row if the gate is open); refill gcur with the row two ahead;
+    // finish the previous row's up dot from uprev (prev_row < 0: none).
+    // Steps past the wave's last row run on dummy data and change nothing.
+    __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC],
+                         u32x4 (&uprev)[NC], int &prev_row) {
+        const float g = dot(gcur);
+        const bool open = valid && g > 0.f;
+        issue(open ? static_cast<const void *>(wu + (size_t)row * H) : dummy, ucur);
+        issue(next2 >= 0 ? static_cast<const void *>(wg + (size_t)next2 * H) : dummy, gcur);
+        if (lane == 0 && valid) {
+            s_g[row] = g;
+            s_on[row] = 0;
+            s_h[row] = 0.f;
+        }
+        if (prev_row >= 0) {
+            const float u = dot(uprev);
+            if (lane == 0 && u > 0.f) {
+                s_on[prev_row] = 1;
+                s_h[prev_row] = s_g[prev_row] * u;
+            }
+        }
+        prev_row = open ? row : -1;
+    }
+};
+
+template <typename WT, int NC, int MR>
+__global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
+    constexpr int CE = WTraits<WT>::CE;
+    constexpr int NCD = (NC * 64 + kThreads - 1) / kThreads;
+
+    __shared__ float s_g[kMaxTile];
+    __shared__ float s_h[kMaxTile];
+    __shared__ int s_on[kMaxTile];
+    __shared__ int s_al[kMaxTile];
+    __shared__ float s_av[kMaxTile];
+    __shared__ int s_n[2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int tile = blockIdx.x % a.ntiles;
+    const int slot = blockIdx.x / a.ntiles;
+    const int tok = slot / a.slots_per_tok;
+    const int n0 = tile * a.tile;
+    const int nt = min(a.tile, a.I - n0);
+    const int H = a.H;
+    const int nch = H / CE;
+    const size_t pr = (size_t)slot * a.ntiles + tile;
+
+    size_t eoff = 0;
+    if (a.route) eoff = (size_t)a.route[slot] * a.expert_stride;
+    const WT *wg = reinterpret_cast<const WT *>(a.wg) + eoff + (size_t)n0 * H;
+    const WT *wu = reinterpret_cast<const WT *>(a.wu) + eoff + (size_t)n0 * H;
+    const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff + (size_t)n0 * H;
+
+    float xr[NC][CE];
+    const float *xt = a.x + (size_t)tok * H;
+    PipeWave<WT, NC> pw{wg, wu, xt, H, nch, lane, xr, s_g, s_h, s_on};
+
+    // this wave's rows: wave, wave + 8, ...; first two gate rows in flight
+    const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
+    u32x4 g0[NC], g1[NC], u0[NC], u1[NC];
+    load_x<WT, NC>(xt, lane, nch, xr);
+    pw.issue(nrow > 0 ? static_cast<const void *>(wg + (size_t)wave * H) : xt, g0);
+    pw.issue(nrow > 1 ? static_cast<const void *>(wg + (size_t)(wave + kWaves) * H) : xt, g1);
+
+    // MR (even) >= rows per wave; the loop is unrolled so every load is
+    // issued in straight-line code.
+    int prev = -1;
+#pragma unroll
+    for (int i = 0; i < MR; i += 2) {
+        const int r = wave + kWaves * i;
+        pw.step(r, i < nrow, i + 2 < nrow ? r + 2 * kWaves : -1, g0, u0, u1, prev);
+        pw.step(r + kWaves, i + 1 < nrow, i + 3 < nrow ? r + 3 * kWaves : -1, g1, u1, u0, prev);
+    }
+    if (prev >= 0) {  // the last step's up loads sit in u1
+        const float u = pw.dot(u1);
+        if (lane == 0 && u > 0.f) {
+            s_on[prev] = 1;
+            s_h[prev] = s_g[prev] * u;
+        }
+    }
+    __syncthreads();
+
+    // ---- ballots: open gates (report) and non-zero Combined activations ------
+    if (wave == 0) {
+        const bool in = lane < nt;
+        const bool pg = in && s_g[lane] > 0.f;
+        const uint64_t mg = __ballot(pg);
+        if (pg && a.want_seg) a.gseg[pr * a.tile + lane_prefix(mg, lane)] = n0 + lane;
+        const bool pa = in && s_on[lane];
+        const uint64_t ma = __ballot(pa);
+        if (pa) {
+            const int pos = lane_prefix(ma, lane);
+            s_al[pos] = lane;
+            s_av[pos] = s_h[lane];
+            if (a.want_seg) a.aseg[pr * a.tile + pos] = n0 + lane;
+        }
+        if (lane == 0) {
+            s_n[0] = __popcll(mg);
+            s_n[1] = __popcll(ma);
+        }
+    }
+    __syncthreads();
+    const int na = s_n[1];
+
+    // ---- down: axpy over the W_down_t rows of A, hidden split over threads --
+    float acc[NCD][CE];
+#pragma unroll
+    for (int kd = 0; kd < NCD; ++kd)
+#pragma unroll
+        for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
+    for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
+        u32x4 v[kDownUnroll][NCD];
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const int aa = a0 + u;
+            const WT *row = wd + (size_t)s_al[aa < na ? aa : a0] * H;
+#pragma unroll
+            for (int kd = 0; kd < NCD; ++kd)
+                v[u][kd] = ld_stream_masked(row, tid + kThreads * kd, nch, 16, aa < na);
+        }
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
+#pragma unroll
+            for (int kd = 0; kd < NCD; ++kd) {
+                float f[CE];
+                unpack<WT>(v[u][kd], f);
+#pragma unroll
+                for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
+            }
+        }
+    }
+    float *prow = a.partial + pr * H;
+#pragma unroll
+    for (int kd = 0; kd < NCD; ++kd) {
+        const int c = tid + kThreads * kd;
+        if (c < nch) {
+#pragma unroll
+            for (int e = 0; e < CE; e += 4)
+                *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
+                    f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
+        }
+    }
+    if (tid == 0) {
+        a.cnt[pr * 2] = s_n[0];
+        a.cnt[pr * 2 + 1] = na;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Split path, kernel 1: gate GEMV + ReLU + ballot compaction and the gathered
+// up rows for a tile of `tile` neurons per 4-wave workgroup.  Output per tile:
+// |G|, |A|, the ascending A segment with its Combined values (and the G
+// segment when a report is requested).
+
+struct GateArgs {
+    const float *x;
+    const void *wg;
+    const void *wu;
+    const int32_t *route;
+    size_t expert_stride;
+    int H, I, tile, ntiles, slots_per_tok;
+    int32_t *cnt;     // [slots][ntiles][2]
+    int32_t *gseg;    // [slots][ntiles][tile]
+    int32_t *aseg;    // [slots][ntiles][tile]
+    float *hseg;      // [slots][ntiles][tile]
+    int want_gseg;
+};
+
+template <typename WT, int NC, int RIF>
+__global__ __launch_bounds__(kGateThreads) void ffn_gate_up(GateArgs a) {
+    constexpr int CE = WTraits<WT>::CE;
+
+    __shared__ float s_g[kMaxTile];
+    __shared__ float s_h[kMaxTile];
+    __shared__ int s_on[kMaxTile];
+    __shared__ int s_gl[kMaxTile];
+    __shared__ int s_ng;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int tile = blockIdx.x % a.ntiles;
+    const int slot = blockIdx.x / a.ntiles;
+    const int tok = slot / a.slots_per_tok;
+    const int n0 = tile * a.tile;
+    const int nt = min(a.tile, a.I - n0);
+    const int H = a.H;
+    const int nch = H / CE;
+
+    size_t eoff = 0;
+    if (a.route) eoff = (size_t)a.route[slot] * a.expert_stride;
+    const WT *wg = reinterpret_cast<const WT *>(a.wg) + eoff + (size_t)n0 * H;
+    const WT *wu = reinterpret_cast<const WT *>(a.wu) + eoff + (size_t)n0 * H;
+
+    float xr[NC][CE];
+    load_x<WT, NC>(a.x + (size_t)tok * H, lane, nch, xr);
+
+    for (int r = wave; r < nt; r += RIF * kGateWaves) {
+        const WT *rows[RIF];
+        bool valid[RIF];
+#pragma unroll
+        for (int k = 0; k < RIF; ++k) {
+            valid[k] = r + k * kGateWaves < nt;
+            rows[k] = wg + (size_t)(valid[k] ? r + k * kGateWaves : r) * H;
+        }
+        float d[RIF];
+        dot_rows<WT, NC, RIF>(rows, valid, xr, lane, nch, d);
+        if (lane == 0) {
+#pragma unroll
+            for (int k = 0; k < RIF; ++k)
+                if (valid[k]) s_g[r + k * kGateWaves] = d[k];
+        }
+    }
+    __syncthreads();
+
+    const size_t pr = (size_t)slot * a.ntiles + tile;
+    if (wave == 0) {
+        const bool p = lane < nt && s_g[lane] > 0.f;
+        const uint64_t m = __ballot(p);
+        if (p) {
+            const int pos = lane_prefix(m, lane);
+            s_gl[pos] = lane;
+            if (a.want_gseg) a.gseg[pr * a.tile + pos] = n0 + lane;
+        }
+        if (lane == 0) s_ng = __popcll(m);
+    }
+    __syncthreads();
+    const int ng = s_ng;
+
+    for (int q = wave; q < ng; q += RIF * kGateWaves) {
+        const WT *rows[RIF];
+        bool valid[RIF];
+        int li[RIF];
+#pragma unroll
+        for (int k = 0; k < RIF; ++k) {
+            valid[k] = q + k * kGateWaves < ng;
+            li[k] = s_gl[valid[k] ? q + k * kGateWaves : q];
+            rows[k] = wu + (size_t)li[k] * H;
+        }
+        float u[RIF];
+        dot_rows<WT, NC, RIF>(rows, valid, xr, lane, nch, u);
+        if (lane == 0) {
+#pragma unroll
+            for (int k = 0; k < RIF; ++k) {
+                if (valid[k]) {
+                    const float g = s_g[li[k]];
+                    const bool on = u[k] > 0.f;  // g > 0 holds for every member of G
+                    s_on[q + k * kGateWaves] = on;
+                    s_h[q + k * kGateWaves] = on ? g * u[k] : 0.f;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    if (wave == 0) {
+        const bool p = lane < ng && s_on[lane];
+        const uint64_t m = __ballot(p);
+        if (p) {
+            const int pos = lane_prefix(m, lane);
+            a.aseg[pr * a.tile + pos] = n0 + s_gl[lane];
+            a.hseg[pr * a.tile + pos] = s_h[lane];
+        }
+        if (lane == 0) {
+            a.cnt[pr * 2] = ng;
+            a.cnt[pr * 2 + 1] = __popcll(m);
+        }
+    }
+}
+
+// Split path, kernel 2: the down projection over A.  Workgroup (slot, chunk,
+// slice): `chunk` is a run of `tpc` consecutive gate+up tiles, `slice` a run
+// of 64 16-byte column chunks.  The workgroup lists the chunk's active rows
+// (ascending) in LDS, its 4 waves accumulate Combined_i * W_down_t[i][slice]
+// over them (rows w, w+4, ...; eight loads in flight per lane), the waves'
+// sums are added in a fixed order and stored as the chunk's partial row.
+
+struct DownArgs {
+    const void *wd;
+    const int32_t *route;
+    size_t expert_stride;
+    int H, tile, ntiles, nslices, nchunks, tpc;
+    const int32_t *cnt;
+    const int32_t *aseg;
+    const float *hseg;
+    float *partial;        // [slots][nchunks][H]
+};
+
+constexpr int kDownWaves = kDownThreads / 64;
+
+template <typename WT>
+__global__ __launch_bounds__(kDownThreads) void ffn_down(DownArgs a) {
+    constexpr int CE = WTraits<WT>::CE;
+    constexpr int SW = 64 * CE;  // columns per slice
+
+    __shared__ int s_row[kDownMaxRows];
+    __shared__ float s_hv[kDownMaxRows];
+    __shared__ int s_cnt[kDownMaxTiles];
+    __shared__ int s_toff[kDownMaxTiles + 1];
+    __shared__ float s_red[kDownWaves][SW];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int slice = blockIdx.x % a.nslices;
+    const int chunk = (blockIdx.x / a.nslices) % a.nchunks;
+    const int slot = blockIdx.x / (a.nslices * a.nchunks);
+    const int H = a.H;
+    const int nch = H / CE;
+    const int t0 = chunk * a.tpc;
+    const int ntc = min(a.tpc, a.ntiles - t0);
+    const size_t tbase = (size_t)slot * a.ntiles + t0;
+
+    // 1. the chunk's active rows: counts, offsets, then one pass of copies
+    for (int t = tid; t < ntc; t += kDownThreads) s_cnt[t] = a.cnt[(tbase + t) * 2 + 1];
+    __syncthreads();
+    if (tid == 0) {
+        int off = 0;
+        for (int t = 0; t < ntc; ++t) {
+            s_toff[t] = off;
+            off += s_cnt[t];
+        }
+        s_toff[ntc] = off;
+    }
+    __syncthreads();
+    for (int e = tid; e < ntc * a.tile; e += kDownThreads) {
+        const int t = e / a.tile, q = e - t * a.tile;
+        if (q < s_cnt[t]) {
+            s_row[s_toff[t] + q] = a.aseg[(tbase + t) * a.tile + q];
+            s_hv[s_toff[t] + q] = a.hseg[(tbase + t) * a.tile + q];
+        }
+    }
+    __syncthreads();
+    const int nrows = s_toff[ntc];
+
+    // 2. axpy over the rows
+    size_t eoff = 0;
+    if (a.route) eoff = (size_t)a.route[slot] * a.expert_stride;
+    const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff;
+    const int c = slice * 64 + lane;
+    float acc[CE];
+#pragma unroll
+    for (int e = 0; e < CE; ++e) acc[e] = 0.f;
+    for (int j0 = wave; j0 < nrows; j0 += kDownUnroll * kDownWaves) {
+        u32x4 v[kDownUnroll];
+        float hv[kDownUnroll];
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const int j = j0 + u * kDownWaves;
+            const bool ok = j < nrows;
+            v[u] = ld_stream_masked(wd + (size_t)s_row[ok ? j : j0] * H, c, nch, 16, ok);
+            hv[u] = ok ? s_hv[j] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            float f[CE];
+            unpack<WT>(v[u], f);
+#pragma unroll
+            for (int e = 0; e < CE; ++e) acc[e] = fmaf(hv[u], f[e], acc[e]);
+        }
+    }
+
+    // 3. waves -> the chunk's partial row slice (wave order fixed)
+#pragma unroll
+    for (int e = 0; e < CE; ++e) s_red[wave][lane * CE + e] = acc[e];
+    __syncthreads();
+    float *prow = a.partial + ((size_t)slot * a.nchunks + chunk) * H;
+    for (int i = tid; i < SW; i += kDownThreads) {
+        const int col = slice * SW + i;
+        float v = s_red[0][i];
+#pragma unroll
+        for (int w = 1; w < kDownWaves; ++w) v += s_red[w][i];
+        if (col < H) prow[col] = v;
+    }
+}
+
+// out[o][:] = sum over the slots s of output row o (ascending), of w_s times
+// the sum over rows r of partial[s][r][:]; w_s = 1 without routing.
+// Block: 16 columns (4 float4) x 64 row groups; a thread adds rows grp,
+// grp + 64, ... in order, the 64 shares are combined by a fixed LDS tree.
+// Grid (column blocks, outputs): 256 workgroups for hidden 4096, so the
+// partial rows stream in one round trip.
+constexpr int kRedCols4 = 4;
+constexpr int kRedGroups = 64;
+constexpr int kRedUnroll = 4;
+
+__global__ __launch_bounds__(256) void ffn_reduce(const float *__restrict__ partial, int rows, int H,
+                                                  int slots_per_out, const float *__restrict__ slot_w,
+                                                  float *__restrict__ out) {
     __shared__ f32x4 red[kRedGroups][kRedCols4];
     const int o = blockIdx.y;
     const int q = threadIdx.x % kRedCols4;
     const int grp = threadIdx.x / kRedCols4;
     const int c4 = blockIdx.x * kRedCols4 + q;
     const int nq = H / 4;
-    const int nrows = slots_per_out * ntiles;
+    const int total = slots_per_out * rows;
+    const size_t base = (size_t)o * slots_per_out * rows;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (c4 < nq) {
-        for (int r0 = grp; r0 < nrows; r0 += 4 * kRedGroups) {
-            int act[4];
-            size_t prs[4];
+    for (int p0 = grp; p0 < total; p0 += kRedUnroll * kRedGroups) {
+        f32x4 v[kRedUnroll];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int r = r0 + u * kRedGroups;
-                const size_t s = (size_t)o * slots_per_out + (r / ntiles);
-                prs[u] = s * ntiles + (r % ntiles);
-                act[u] = r < nrows ? cnt[prs[u] * 2 + 1] : 0;
-            }
-            f32x4 v[4];
+        for (int u = 0; u < kRedUnroll; ++u) {
+            const int p = p0 + u * kRedGroups;
+            const bool ok = p < total;
+            const f32x4 t = ld_f32x4_masked(partial + (base + (ok ? p : p0)) * H, c4, nq);
+            v[u] = ok ? t : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-                v[u] = act[u] > 0 ? *reinterpret_cast<const f32x4 *>(partial + prs[u] * H + c4 * 4)
-                                  : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                if (act[u] > 0) {
-                    const float w = slot_w ? slot_w[prs[u] / ntiles] : 1.f;
-                    acc.x = fmaf(w, v[u].x, acc.x);
-                    acc.y = fmaf(w, v[u].y, acc.y);
-                    acc.z = fmaf(w, v[u].z, acc.z);
-                    acc.w = fmaf(w, v[u].w, acc.w);
-                }
-            }
+        for (int u = 0; u < kRedUnroll; ++u) {
+            const int p = p0 + u * kRedGroups;
+            const float w = (slot_w && p < total) ? slot_w[o * slots_per_out + p / rows] : 1.f;
+            acc.x = fmaf(w, v[u].x, acc.x);
+            acc.y = fmaf(w, v[u].y, acc.y);
+            acc.z = fmaf(w, v[u].z, acc.z);
+            acc.w = fmaf(w, v[u].w, acc.w);
         }
     }
     red[grp][q] = acc;
@@ -458,37 +878,169 @@ __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, c
 
 namespace {
 
-template <typename WT, bool DENSE>
-void launch_main_nc(int nc, dim3 grid, hipStream_t st, const SlotArgs &a) {
-    switch (nc) {
-    case 1: hipLaunchKernelGGL((ffn_slot_main<WT, 1, DENSE>), grid, dim3(kThreads), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((ffn_slot_main<WT, 2, DENSE>), grid, dim3(kThreads), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((ffn_slot_main<WT, 4, DENSE>), grid, dim3(kThreads), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((ffn_slot_main<WT, 8, DENSE>), grid, dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((ffn_slot_main<WT, 16, DENSE>), grid, dim3(kThreads), 0, st, a); break;
-    }
-}
-
-void launch_main(ts_dtype dt, bool dense, const SlotPlan &p, hipStream_t st, const SlotArgs &a) {
-    dim3 grid((unsigned)(p.slots * p.ntiles));
-    if (dt == TS_F32) {
-        if (dense) launch_main_nc<float, true>(p.nc, grid, st, a);
-        else launch_main_nc<float, false>(p.nc, grid, st, a);
-    } else {
-        if (dense) launch_main_nc<uint16_t, true>(p.nc, grid, st, a);
-        else launch_main_nc<uint16_t, false>(p.nc, grid, st, a);
-    }
-}
-
 template <typename T>
 T *ws_at(void *ws, size_t off) {
     return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
 }
 
-// The single-token path over `p.slots` slots: main, reduce, optional report.
-ts_status run_slots(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
+// Rows in flight per wave in the row dot products: 2 by default, 1 when x
+// alone takes 128 registers (NC = 16) or when tuned so.
+int rows_in_flight(int nc) {
+    const int t = tuned("rif");
+    if (nc >= 16) return 1;
+    return t == 1 ? 1 : 2;
+}
+
+template <typename WT, int NC, bool DENSE>
+void launch_fused_rif(int rif, dim3 grid, hipStream_t st, const SlotArgs &a) {
+    if (rif == 1) hipLaunchKernelGGL((ffn_fused<WT, NC, DENSE, 1>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((ffn_fused<WT, NC, DENSE, 2>), grid, dim3(kThreads), 0, st, a);
+}
+
+template <typename WT, bool DENSE>
+void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs &a) {
+    switch (nc) {
+    case 1: launch_fused_rif<WT, 1, DENSE>(rif, grid, st, a); break;
+    case 2: launch_fused_rif<WT, 2, DENSE>(rif, grid, st, a); break;
+    case 4: launch_fused_rif<WT, 4, DENSE>(rif, grid, st, a); break;
+    case 8: launch_fused_rif<WT, 8, DENSE>(rif, grid, st, a); break;
+    default: hipLaunchKernelGGL((ffn_fused<WT, 16, DENSE, 1>), grid, dim3(kThreads), 0, st, a); break;
+    }
+}
+
+// The pipelined kernel keeps x, two gate rows and two up rows in registers;
+// with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
+// The pipelined kernel keeps x, two gate rows and two up rows in registers;
+// with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
+// MR, the unrolled rows per wave, is the smallest of 2, 4, 8 covering the tile.
+template <typename WT, int NC>
+void launch_pipe_mr(int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
+    const int rows = (tile + kWaves - 1) / kWaves;
+    if (rows <= 2) hipLaunchKernelGGL((ffn_pipe<WT, NC, 2>), grid, dim3(kThreads), 0, st, a);
+    else if (rows <= 4) hipLaunchKernelGGL((ffn_pipe<WT, NC, 4>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((ffn_pipe<WT, NC, 8>), grid, dim3(kThreads), 0, st, a);
+}
+
+template <typename WT>
+void launch_pipe(int nc, int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
+    switch (nc) {
+    case 1: launch_pipe_mr<WT, 1>(tile, grid, st, a); break;
+    case 2: launch_pipe_mr<WT, 2>(tile, grid, st, a); break;
+    case 4: launch_pipe_mr<WT, 4>(tile, grid, st, a); break;
+    default: launch_pipe_mr<WT, 8>(tile, grid, st, a); break;
+    }
+}
+
+template <typename WT, int NC>
+void launch_gate_up_rif(int rif, dim3 grid, hipStream_t st, const GateArgs &a) {
+    if (rif == 1) hipLaunchKernelGGL((ffn_gate_up<WT, NC, 1>), grid, dim3(kGateThreads), 0, st, a);
+    else hipLaunchKernelGGL((ffn_gate_up<WT, NC, 2>), grid, dim3(kGateThreads), 0, st, a);
+}
+
+template <typename WT>
+void launch_gate_up(int nc, int rif, dim3 grid, hipStream_t st, const GateArgs &a) {
+    switch (nc) {
+    case 1: launch_gate_up_rif<WT, 1>(rif, grid, st, a); break;
+    case 2: launch_gate_up_rif<WT, 2>(rif, grid, st, a); break;
+    case 4: launch_gate_up_rif<WT, 4>(rif, grid, st, a); break;
+    case 8: launch_gate_up_rif<WT, 8>(rif, grid, st, a); break;
+    default: hipLaunchKernelGGL((ffn_gate_up<WT, 16, 1>), grid, dim3(kGateThreads), 0, st, a); break;
+    }
+}
+
+ts_status launch_reduce(const float *partial, int rows, const SlotPlan &p, const float *slot_w, float *out,
+                        hipStream_t st) {
+    ProfScope ps("ffn_reduce", st);
+    dim3 grid((unsigned)((p.hidden / 4 + kRedCols4 - 1) / kRedCols4), (unsigned)p.outs);
+    hipLaunchKernelGGL(ffn_reduce, grid, dim3(256), 0, st, partial, rows, p.hidden, p.slots_per_out, slot_w, out);
+    return check_launch("ffn_reduce");
+}
+
+ts_status run_report(const SlotPlan &p, const int32_t *cnt, const int32_t *gseg, const int32_t *aseg, int ntiles,
+                     int tile, const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+    if (!stats) return TS_OK;
+    if (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx) {
+        ProfScope ps("ffn_stats", st);
+        hipLaunchKernelGGL(ffn_stats, dim3((unsigned)p.slots), dim3(256), 0, st, cnt, gseg, aseg, ntiles, tile,
+                           p.inter, stats->n_gate, stats->n_active, stats->gate_idx, stats->active_idx);
+        ts_status s = check_launch("ffn_stats");
+        if (s != TS_OK) return s;
+    }
+    if (stats->n_union) {
+        int32_t *flags = ws_at<int32_t>(ws, p.off_aux);
+        ProfScope ps("ffn_stats", st);
+        hipLaunchKernelGGL(fill_i32, dim3(64), dim3(256), 0, st, flags, (size_t)2 * p.inter, 0);
+        hipLaunchKernelGGL(ffn_union_mark, dim3(256), dim3(256), 0, st, cnt, gseg, aseg, ntiles, tile, p.slots,
+                           p.inter, flags);
+        hipLaunchKernelGGL(ffn_union_count, dim3(1), dim3(256), 0, st, flags, p.inter, stats->n_union);
+        ts_status s = check_launch("ffn_union");
+        if (s != TS_OK) return s;
+    }
+    return TS_OK;
+}
+
+// Split sparse path over `p.slots` slots: gate+up, down, reduce, report.
+ts_status run_split(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
+                    size_t expert_stride, ts_dtype dt, const SlotPlan &p, float *out, const float *slot_w,
+                    const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+    const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
+    GateArgs g;
+    g.x = x;
+    g.wg = wg;
+    g.wu = wu;
+    g.route = route;
+    g.expert_stride = expert_stride;
+    g.H = p.hidden;
+    g.I = p.inter;
+    g.tile = p.gtile;
+    g.ntiles = p.gntiles;
+    g.slots_per_tok = p.slots_per_out;
+    g.cnt = ws_at<int32_t>(ws, p.off_gcnt);
+    g.gseg = ws_at<int32_t>(ws, p.off_ggseg);
+    g.aseg = ws_at<int32_t>(ws, p.off_gaseg);
+    g.hseg = ws_at<float>(ws, p.off_ghseg);
+    g.want_gseg = want_seg ? 1 : 0;
+    {
+        ProfScope ps("ffn_gate_up", st);
+        dim3 grid((unsigned)(p.slots * p.gntiles));
+        const int rif = rows_in_flight(p.nc);
+        if (dt == TS_F32) launch_gate_up<float>(p.nc, rif, grid, st, g);
+        else launch_gate_up<uint16_t>(p.nc, rif, grid, st, g);
+    }
+    ts_status s = check_launch("ffn_gate_up");
+    if (s != TS_OK) return s;
+    DownArgs d;
+    d.wd = wd;
+    d.route = route;
+    d.expert_stride = expert_stride;
+    d.H = p.hidden;
+    d.tile = p.gtile;
+    d.ntiles = p.gntiles;
+    d.nslices = p.nslices;
+    d.nchunks = p.nchunks;
+    d.tpc = p.tpc;
+    d.cnt = g.cnt;
+    d.aseg = g.aseg;
+    d.hseg = g.hseg;
+    d.partial = ws_at<float>(ws, p.off_dpartial);
+    {
+        ProfScope ps("ffn_down", st);
+        dim3 grid((unsigned)(p.slots * p.nchunks * p.nslices));
+        if (dt == TS_F32) hipLaunchKernelGGL(ffn_down<float>, grid, dim3(kDownThreads), 0, st, d);
+        else hipLaunchKernelGGL(ffn_down<uint16_t>, grid, dim3(kDownThreads), 0, st, d);
+    }
+    s = check_launch("ffn_down");
+    if (s != TS_OK) return s;
+    s = launch_reduce(d.partial, p.nchunks, p, slot_w, out, st);
+    if (s != TS_OK) return s;
+    return run_report(p, g.cnt, g.gseg, g.aseg, p.gntiles, p.gtile, stats, ws, st);
+}
+
+// Fused single-token path (the dense comparator, and the default sparse
+// path): one workgroup per tile runs gate, up and down, then ffn_reduce.
+ts_status run_fused(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
                     size_t expert_stride, ts_dtype dt, bool dense, const SlotPlan &p, float *out,
-                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool pipe) {
     const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
     SlotArgs a;
     a.x = x;
@@ -509,36 +1061,34 @@ ts_status run_slots(const float *x, const void *wg, const void *wu, const void *
     a.want_seg = want_seg ? 1 : 0;
     {
         ProfScope ps("ffn_main", st);
-        launch_main(dt, dense, p, st, a);
+        dim3 grid((unsigned)(p.slots * p.ntiles));
+        const int rif = rows_in_flight(p.nc);
+        if (pipe && p.nc <= 8) {
+            if (dt == TS_F32) launch_pipe<float>(p.nc, p.tile, grid, st, a);
+            else launch_pipe<uint16_t>(p.nc, p.tile, grid, st, a);
+        } else if (dt == TS_F32) {
+            if (dense) launch_fused_nc<float, true>(p.nc, rif, grid, st, a);
+            else launch_fused_nc<float, false>(p.nc, rif, grid, st, a);
+        } else {
+            if (dense) launch_fused_nc<uint16_t, true>(p.nc, rif, grid, st, a);
+            else launch_fused_nc<uint16_t, false>(p.nc, rif, grid, st, a);
+        }
     }
     ts_status s = check_launch("ffn_main");
     if (s != TS_OK) return s;
-    {
-        ProfScope ps("ffn_reduce", st);
-        dim3 grid((unsigned)((p.hidden / 4 + kRedCols4 - 1) / kRedCols4), (unsigned)p.outs);
-        hipLaunchKernelGGL(ffn_reduce, grid, dim3(256), 0, st, a.partial, a.cnt, p.ntiles, p.hidden,
-                           p.slots_per_out, slot_w, out);
-    }
-    s = check_launch("ffn_reduce");
+    s = launch_reduce(a.partial, p.ntiles, p, slot_w, out, st);
     if (s != TS_OK) return s;
-    if (stats && (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx)) {
-        ProfScope ps("ffn_stats", st);
-        hipLaunchKernelGGL(ffn_stats, dim3((unsigned)p.slots), dim3(256), 0, st, a.cnt, a.gseg, a.aseg, p.ntiles,
-                           p.tile, p.inter, stats->n_gate, stats->n_active, stats->gate_idx, stats->active_idx);
-        s = check_launch("ffn_stats");
-        if (s != TS_OK) return s;
-    }
-    if (stats && stats->n_union) {
-        int32_t *flags = ws_at<int32_t>(ws, p.off_aux);
-        ProfScope ps("ffn_stats", st);
-        hipLaunchKernelGGL(fill_i32, dim3(64), dim3(256), 0, st, flags, (size_t)2 * p.inter, 0);
-        hipLaunchKernelGGL(ffn_union_mark, dim3(256), dim3(256), 0, st, a.cnt, a.gseg, a.aseg, p.ntiles, p.tile,
-                           p.slots, p.inter, flags);
-        hipLaunchKernelGGL(ffn_union_count, dim3(1), dim3(256), 0, st, flags, p.inter, stats->n_union);
-        s = check_launch("ffn_union");
-        if (s != TS_OK) return s;
-    }
-    return TS_OK;
+    return run_report(p, a.cnt, a.gseg, a.aseg, p.ntiles, p.tile, stats, ws, st);
+}
+
+ts_status run_slots(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
+                    size_t expert_stride, ts_dtype dt, bool dense, const SlotPlan &p, float *out,
+                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+    const int path = tuned("ffn_path");
+    if (dense || path == 2)
+        return run_fused(x, wg, wu, wd, route, expert_stride, dt, dense, p, out, slot_w, stats, ws, st, false);
+    if (path == 1) return run_split(x, wg, wu, wd, route, expert_stride, dt, p, out, slot_w, stats, ws, st);
+    return run_fused(x, wg, wu, wd, route, expert_stride, dt, false, p, out, slot_w, stats, ws, st, true);
 }
 
 ts_status check_ffn_args(const float *x, const void *wg, const void *wu, const void *wd, ts_dtype dt, int batch,

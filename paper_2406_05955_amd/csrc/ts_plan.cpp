@@ -9,12 +9,25 @@ namespace ts {
 
 namespace {
 std::atomic<int> g_tile{0};
+std::atomic<int> g_gate_tile{0};
+std::atomic<int> g_down_chunks{0};
+std::atomic<int> g_path{0};
+std::atomic<int> g_rif{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
 }  // namespace
 
 int tuned_tile() { return g_tile.load(); }
+
+int tuned(const char *key) {
+    if (std::strcmp(key, "ffn_tile") == 0) return g_tile.load();
+    if (std::strcmp(key, "gate_tile") == 0) return g_gate_tile.load();
+    if (std::strcmp(key, "down_chunks") == 0) return g_down_chunks.load();
+    if (std::strcmp(key, "ffn_path") == 0) return g_path.load();
+    if (std::strcmp(key, "rif") == 0) return g_rif.load();
+    return 0;
+}
 
 // Neurons per workgroup for the single-token kernel: enough workgroups to
 // give every compute unit one (256 on MI355X), rounded to a multiple of 8
@@ -91,6 +104,41 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     off = align256(off + (size_t)slots * sizeof(float));
     q.off_aux = off;  // union flags of the activity report: [2][inter]
     off = align256(off + (size_t)2 * (size_t)inter * sizeof(int32_t));
+
+    // Split path.  Gate+up tiles: about three 4-wave workgroups per compute
+    // unit over all slots, a multiple of 4 rows (one share per wave).
+    int gt = g_gate_tile.load();
+    if (gt <= 0) {
+        long long per = ((long long)inter * slots + kGateTargetBlocks - 1) / kGateTargetBlocks;
+        per = (per + 3) / 4 * 4;
+        gt = (int)std::min<long long>(kMaxTile, std::max<long long>(8, per));
+    }
+    q.gtile = gt;
+    q.gntiles = (inter + gt - 1) / gt;
+    // Down: 64 chunks of 16 bytes per slice; chunks of tiles sized so that a
+    // chunk's rows fit the LDS list and there are ~256 workgroups in all.
+    q.nslices = (q.nch + 63) / 64;
+    // tpc * gt <= kDownMaxRows and tpc <= kDownMaxTiles bound the LDS lists.
+    int want = g_down_chunks.load();
+    if (want <= 0) want = std::max(1, kDownTargetBlocks / std::max(1, q.nslices * slots));
+    int nchunks = std::max(1, std::min(want, q.gntiles));
+    int tpc = (q.gntiles + nchunks - 1) / nchunks;
+    tpc = std::min(tpc, std::min(kDownMaxTiles, kDownMaxRows / gt));
+    q.tpc = std::max(1, tpc);
+    q.nchunks = (q.gntiles + q.tpc - 1) / q.tpc;
+    size_t gst = (size_t)slots * (size_t)q.gntiles;
+    q.off_gcnt = off;
+    off = align256(off + gst * 2 * sizeof(int32_t));
+    q.off_ggseg = off;
+    off = align256(off + gst * (size_t)gt * sizeof(int32_t));
+    q.off_gaseg = off;
+    off = align256(off + gst * (size_t)gt * sizeof(int32_t));
+    q.off_ghseg = off;
+    off = align256(off + gst * (size_t)gt * sizeof(float));
+    q.off_dpartial = off;
+    off = align256(off + (size_t)slots * q.nchunks * (size_t)hidden * sizeof(float));
+    q.off_ctr = off;
+    off = align256(off + (size_t)q.outs * q.nslices * sizeof(int32_t));
     q.total = off;
     *p = q;
     return true;
@@ -152,8 +200,28 @@ size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, i
 ts_status ts_tune_set(const char *key, int value) {
     if (!key) return TS_ERR_NULL;
     if (std::strcmp(key, "ffn_tile") == 0) {
-        if (value != 0 && (value < 8 || value > ts::kMaxTile || value % 8 != 0)) return TS_ERR_SHAPE;
+        if (value != 0 && (value < 4 || value > ts::kMaxTile || value % 4 != 0)) return TS_ERR_SHAPE;
         ts::g_tile.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "gate_tile") == 0) {
+        if (value != 0 && (value < 4 || value > ts::kMaxTile || value % 4 != 0)) return TS_ERR_SHAPE;
+        ts::g_gate_tile.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "down_chunks") == 0) {
+        if (value < 0 || value > 4096) return TS_ERR_SHAPE;
+        ts::g_down_chunks.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "ffn_path") == 0) {
+        if (value < 0 || value > 2) return TS_ERR_SHAPE;
+        ts::g_path.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "rif") == 0) {
+        if (value < 0 || value > 2) return TS_ERR_SHAPE;
+        ts::g_rif.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;

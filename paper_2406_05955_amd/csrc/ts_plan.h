@@ -17,6 +17,13 @@ constexpr int kWaves = 8;                 // waves per workgroup of the single-t
 constexpr int kThreads = kWaves * 64;     // 512 threads
 constexpr int kMaxTile = 64;              // neurons per workgroup: one wave ballot covers the tile
 constexpr int kTargetTiles = 256;         // one workgroup per compute unit on MI355X
+constexpr int kGateWaves = 4;             // waves per workgroup of the gate+up kernel
+constexpr int kGateThreads = kGateWaves * 64;
+constexpr int kGateTargetBlocks = 768;    // three 4-wave workgroups per compute unit
+constexpr int kDownThreads = 256;         // 4 waves per down workgroup
+constexpr int kDownMaxRows = 1024;        // active rows one down workgroup can list in LDS
+constexpr int kDownTargetBlocks = 256;
+constexpr int kDownMaxTiles = 256;        // gate+up tiles one down workgroup can list
 
 // Workspace layout and launch shape shared by the single-token path (one
 // "slot" = one (token, expert) pair processed against one weight set).
@@ -30,9 +37,16 @@ struct SlotPlan {
     int slots = 0;     // number of slots
     int outs = 0;      // output rows (slots / slots_per_out)
     int slots_per_out = 1;
+    // split sparse path: gate+up kernel tiles and down kernel decomposition
+    int gtile = 0;     // neurons per gate+up workgroup
+    int gntiles = 0;   // gate+up workgroups per slot
+    int nslices = 0;   // column slices of the down kernel (64 chunks of 16 bytes each)
+    int nchunks = 0;   // groups of gate+up tiles per slot in the down kernel
+    int tpc = 0;       // gate+up tiles per chunk
     // byte offsets into the workspace
     size_t off_cnt = 0, off_gseg = 0, off_aseg = 0, off_partial = 0;
     size_t off_route_idx = 0, off_route_w = 0, off_aux = 0;
+    size_t off_gcnt = 0, off_ggseg = 0, off_gaseg = 0, off_ghseg = 0, off_dpartial = 0, off_ctr = 0;
     size_t total = 0;
 };
 
@@ -51,6 +65,7 @@ struct BatchPlan {
 
 int tuned_tile();
 int choose_tile(int inter);
+int tuned(const char *key);
 bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p);
 bool plan_batch(int batch, int hidden, int inter, ts_dtype dt, BatchPlan *p);
 

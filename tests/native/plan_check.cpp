@@ -1,0 +1,62 @@
+// Host-only check of the launch planner's invariants over a grid of shapes.
+// Built with g++ (sanitizers on) by tests/test_plan_cpu.py; prints "ok" or
+// the first violated invariant.
+#include <cstdio>
+
+#include "ts_plan.h"
+
+using namespace ts;
+
+static int fail(const char *what, int B, int H, int I, int S) {
+    std::printf("FAIL %s B=%d H=%d I=%d slots=%d\n", what, B, H, I, S);
+    return 1;
+}
+
+int main() {
+    const int Hs[] = {8, 16, 40, 200, 512, 1000, 2048, 4096, 6144, 8192};
+    const int Is[] = {1, 3, 7, 8, 9, 63, 64, 65, 130, 777, 1792, 3001, 14336, 28672, 100000};
+    const int Ss[] = {1, 2, 3, 8, 16, 32, 64, 256, 512, 2048};
+    const int tiles[] = {0, 4, 8, 12, 20, 64};
+    const int chunks[] = {0, 1, 7, 32, 4096};
+    const ts_dtype dts[] = {TS_F32, TS_BF16};
+    for (ts_dtype dt : dts)
+        for (int H : Hs)
+            for (int I : Is)
+                for (int S : Ss)
+                    for (int gt : tiles)
+                        for (int ch : chunks) {
+                            if (ts_tune_set("gate_tile", gt) != TS_OK) return fail("tune gate_tile", 0, H, I, S);
+                            if (ts_tune_set("down_chunks", ch) != TS_OK) return fail("tune down_chunks", 0, H, I, S);
+                            SlotPlan p;
+                            bool ok = plan_slots(H, I, dt, S, 1, &p);
+                            bool valid = check_dims(1, H, I, dt) == TS_OK;
+                            if (ok != valid) return fail("plan/validation disagree", 1, H, I, S);
+                            if (!ok) continue;
+                            if (p.gtile < 4 || p.gtile > kMaxTile || p.gtile % 4) return fail("gtile", 1, H, I, S);
+                            if ((long long)p.gntiles * p.gtile < I || (long long)(p.gntiles - 1) * p.gtile >= I)
+                                return fail("gntiles", 1, H, I, S);
+                            if (p.tpc < 1 || p.tpc > kDownMaxTiles || p.tpc * p.gtile > kDownMaxRows)
+                                return fail("tpc bounds", 1, H, I, S);
+                            if ((long long)p.nchunks * p.tpc < p.gntiles || (long long)(p.nchunks - 1) * p.tpc >= p.gntiles)
+                                return fail("nchunks cover", 1, H, I, S);
+                            if (p.nslices * 64 < p.nch || (p.nslices - 1) * 64 >= p.nch) return fail("nslices", 1, H, I, S);
+                            if (p.nc * 64 < p.nch || p.nc > 16) return fail("nc", 1, H, I, S);
+                            if (p.tile < 8 || p.tile > kMaxTile) return fail("tile", 1, H, I, S);
+                            if ((long long)p.ntiles * p.tile < I) return fail("ntiles", 1, H, I, S);
+                            // workspace regions ordered, aligned and inside total
+                            size_t offs[] = {p.off_cnt, p.off_gseg, p.off_aseg, p.off_partial, p.off_route_idx,
+                                             p.off_route_w, p.off_aux, p.off_gcnt, p.off_ggseg, p.off_gaseg,
+                                             p.off_ghseg, p.off_dpartial, p.off_ctr, p.total};
+                            for (int k = 1; k < 14; ++k)
+                                if (offs[k] < offs[k - 1] || offs[k] % 256) return fail("ws layout", 1, H, I, S);
+                            size_t need_dp = (size_t)S * p.nchunks * H * 4;
+                            if (p.off_ctr - p.off_dpartial < need_dp) return fail("dpartial size", 1, H, I, S);
+                            if (p.total - p.off_ctr < (size_t)p.outs * p.nslices * 4) return fail("ctr size", 1, H, I, S);
+                            if (p.off_gaseg - p.off_ggseg < (size_t)S * p.gntiles * p.gtile * 4)
+                                return fail("gseg size", 1, H, I, S);
+                        }
+    ts_tune_set("gate_tile", 0);
+    ts_tune_set("down_chunks", 0);
+    std::printf("ok\n");
+    return 0;
+}

@@ -107,7 +107,7 @@ def test_probe_checks():
 
 
 def test_tune_checks():
-    assert ts.lib.ts_tune_set(b"ffn_tile", 12) == SHAPE
+    assert ts.lib.ts_tune_set(b"ffn_tile", 10) == SHAPE
     assert ts.lib.ts_tune_set(b"ffn_tile", 72) == SHAPE
     assert ts.lib.ts_tune_set(b"nope", 8) == SHAPE
     assert ts.lib.ts_tune_set(b"ffn_tile", 32) == OK

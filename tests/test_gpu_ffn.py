@@ -163,3 +163,20 @@ def test_error_leaves_output_untouched():
         ts.ffn_sparse(x, wg, wu, wd, out=out, ws=small)
     torch.cuda.synchronize()
     assert torch.all(out == 7.0).item()
+
+
+@pytest.mark.parametrize("path,rif,gtile,chunks", [(0, 0, 0, 0), (2, 1, 0, 0), (2, 2, 0, 0), (1, 2, 0, 0),
+                                                   (1, 1, 16, 0), (1, 2, 64, 7), (1, 2, 8, 4096)])
+@pytest.mark.parametrize("dtype,B,H,I", [(synth.F32, 1, 512, 1792), (synth.BF16, 3, 1000 + 8, 3001),
+                                         (synth.BF16, 1, 4096, 5000), (synth.F32, 2, 40, 65)])
+def test_kernel_variants(path, rif, gtile, chunks, dtype, B, H, I):
+    """Every single-token kernel sequence (pipelined, fused, split gate+up /
+    down) and both rows-in-flight settings give the oracle's result and sets."""
+    for k, v in (("ffn_path", path), ("rif", rif), ("gate_tile", gtile), ("down_chunks", chunks)):
+        ts.tune_set(k, v)
+    try:
+        inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[path, rif, gtile, B, H, I])
+        check_ffn(inp)
+    finally:
+        for k in ("ffn_path", "rif", "gate_tile", "down_chunks"):
+            ts.tune_set(k, 0)
