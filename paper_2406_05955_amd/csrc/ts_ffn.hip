@@ -893,8 +893,8 @@ int rows_in_flight(int nc) {
 
 template <typename WT, int NC, bool DENSE>
 void launch_fused_rif(int rif, dim3 grid, hipStream_t st, const SlotArgs &a) {
-    if (rif == 1) hipLaunchKernelGGL((ffn_fused<WT, NC, DENSE, 1>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((ffn_fused<WT, NC, DENSE, 2>), grid, dim3(kThreads), 0, st, a);
+    if (rif == 1) launch("ffn_main", ffn_fused<WT, NC, DENSE, 1>, grid, dim3(kThreads), st, a);
+    else launch("ffn_main", ffn_fused<WT, NC, DENSE, 2>, grid, dim3(kThreads), st, a);
 }
 
 template <typename WT, bool DENSE>
@@ -904,7 +904,7 @@ void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs 
     case 2: launch_fused_rif<WT, 2, DENSE>(rif, grid, st, a); break;
     case 4: launch_fused_rif<WT, 4, DENSE>(rif, grid, st, a); break;
     case 8: launch_fused_rif<WT, 8, DENSE>(rif, grid, st, a); break;
-    default: hipLaunchKernelGGL((ffn_fused<WT, 16, DENSE, 1>), grid, dim3(kThreads), 0, st, a); break;
+    default: launch("ffn_main", ffn_fused<WT, 16, DENSE, 1>, grid, dim3(kThreads), st, a); break;
     }
 }
 
@@ -916,9 +916,9 @@ void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs 
 template <typename WT, int NC>
 void launch_pipe_mr(int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
     const int rows = (tile + kWaves - 1) / kWaves;
-    if (rows <= 2) hipLaunchKernelGGL((ffn_pipe<WT, NC, 2>), grid, dim3(kThreads), 0, st, a);
-    else if (rows <= 4) hipLaunchKernelGGL((ffn_pipe<WT, NC, 4>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((ffn_pipe<WT, NC, 8>), grid, dim3(kThreads), 0, st, a);
+    if (rows <= 2) launch("ffn_main", ffn_pipe<WT, NC, 2>, grid, dim3(kThreads), st, a);
+    else if (rows <= 4) launch("ffn_main", ffn_pipe<WT, NC, 4>, grid, dim3(kThreads), st, a);
+    else launch("ffn_main", ffn_pipe<WT, NC, 8>, grid, dim3(kThreads), st, a);
 }
 
 template <typename WT>
@@ -933,8 +933,8 @@ void launch_pipe(int nc, int tile, dim3 grid, hipStream_t st, const SlotArgs &a)
 
 template <typename WT, int NC>
 void launch_gate_up_rif(int rif, dim3 grid, hipStream_t st, const GateArgs &a) {
-    if (rif == 1) hipLaunchKernelGGL((ffn_gate_up<WT, NC, 1>), grid, dim3(kGateThreads), 0, st, a);
-    else hipLaunchKernelGGL((ffn_gate_up<WT, NC, 2>), grid, dim3(kGateThreads), 0, st, a);
+    if (rif == 1) launch("ffn_gate_up", ffn_gate_up<WT, NC, 1>, grid, dim3(kGateThreads), st, a);
+    else launch("ffn_gate_up", ffn_gate_up<WT, NC, 2>, grid, dim3(kGateThreads), st, a);
 }
 
 template <typename WT>
@@ -944,15 +944,14 @@ void launch_gate_up(int nc, int rif, dim3 grid, hipStream_t st, const GateArgs &
     case 2: launch_gate_up_rif<WT, 2>(rif, grid, st, a); break;
     case 4: launch_gate_up_rif<WT, 4>(rif, grid, st, a); break;
     case 8: launch_gate_up_rif<WT, 8>(rif, grid, st, a); break;
-    default: hipLaunchKernelGGL((ffn_gate_up<WT, 16, 1>), grid, dim3(kGateThreads), 0, st, a); break;
+    default: launch("ffn_gate_up", ffn_gate_up<WT, 16, 1>, grid, dim3(kGateThreads), st, a); break;
     }
 }
 
 ts_status launch_reduce(const float *partial, int rows, const SlotPlan &p, const float *slot_w, float *out,
                         hipStream_t st) {
-    ProfScope ps("ffn_reduce", st);
     dim3 grid((unsigned)((p.hidden / 4 + kRedCols4 - 1) / kRedCols4), (unsigned)p.outs);
-    hipLaunchKernelGGL(ffn_reduce, grid, dim3(256), 0, st, partial, rows, p.hidden, p.slots_per_out, slot_w, out);
+    launch("ffn_reduce", ffn_reduce, grid, dim3(256), st, partial, rows, p.hidden, p.slots_per_out, slot_w, out);
     return check_launch("ffn_reduce");
 }
 
@@ -1001,7 +1000,6 @@ ts_status run_split(const float *x, const void *wg, const void *wu, const void *
     g.hseg = ws_at<float>(ws, p.off_ghseg);
     g.want_gseg = want_seg ? 1 : 0;
     {
-        ProfScope ps("ffn_gate_up", st);
         dim3 grid((unsigned)(p.slots * p.gntiles));
         const int rif = rows_in_flight(p.nc);
         if (dt == TS_F32) launch_gate_up<float>(p.nc, rif, grid, st, g);
@@ -1024,10 +1022,9 @@ ts_status run_split(const float *x, const void *wg, const void *wu, const void *
     d.hseg = g.hseg;
     d.partial = ws_at<float>(ws, p.off_dpartial);
     {
-        ProfScope ps("ffn_down", st);
         dim3 grid((unsigned)(p.slots * p.nchunks * p.nslices));
-        if (dt == TS_F32) hipLaunchKernelGGL(ffn_down<float>, grid, dim3(kDownThreads), 0, st, d);
-        else hipLaunchKernelGGL(ffn_down<uint16_t>, grid, dim3(kDownThreads), 0, st, d);
+        if (dt == TS_F32) launch("ffn_down", ffn_down<float>, grid, dim3(kDownThreads), st, d);
+        else launch("ffn_down", ffn_down<uint16_t>, grid, dim3(kDownThreads), st, d);
     }
     s = check_launch("ffn_down");
     if (s != TS_OK) return s;
@@ -1060,7 +1057,6 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     a.partial = ws_at<float>(ws, p.off_partial);
     a.want_seg = want_seg ? 1 : 0;
     {
-        ProfScope ps("ffn_main", st);
         dim3 grid((unsigned)(p.slots * p.ntiles));
         const int rif = rows_in_flight(p.nc);
         if (pipe && p.nc <= 8) {
@@ -1136,15 +1132,12 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
     hipStream_t st = static_cast<hipStream_t>(stream);
     int32_t *ridx = ws_at<int32_t>(ws, p.off_route_idx);
     float *rw = ws_at<float>(ws, p.off_route_w);
-    {
-        ProfScope ps("moe_router", st);
-        if (dt == TS_F32)
-            hipLaunchKernelGGL(moe_router<float>, dim3((unsigned)batch), dim3(256), 0, st, x,
-                               static_cast<const float *>(wr), hidden, E, K, ridx, rw);
-        else
-            hipLaunchKernelGGL(moe_router<uint16_t>, dim3((unsigned)batch), dim3(256), 0, st, x,
-                               static_cast<const uint16_t *>(wr), hidden, E, K, ridx, rw);
-    }
+    if (dt == TS_F32)
+        launch("moe_router", moe_router<float>, dim3((unsigned)batch), dim3(256), st, x,
+               static_cast<const float *>(wr), hidden, E, K, ridx, rw);
+    else
+        launch("moe_router", moe_router<uint16_t>, dim3((unsigned)batch), dim3(256), st, x,
+               static_cast<const uint16_t *>(wr), hidden, E, K, ridx, rw);
     s = check_launch("moe_router");
     if (s != TS_OK) return s;
     s = run_slots(x, wg, wu, wd, ridx, (size_t)inter * (size_t)hidden, dt, dense, p, out, rw, stats, ws, st);

@@ -48,11 +48,8 @@ ts_status ts_probe_read(const void *src, size_t bytes, float *sink, void *stream
     if (bytes == 0 || bytes % 16 != 0) return TS_ERR_SHAPE;
     if (!ts::aligned16(src) || !ts::aligned4(sink)) return TS_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    {
-        ts::ProfScope ps("probe_read", st);
-        hipLaunchKernelGGL(ts::probe_read, dim3(ts::kProbeBlocks), dim3(256), 0, st,
-                           static_cast<const ts::u32x4 *>(src), bytes / 16, sink);
-    }
+    ts::launch("probe_read", ts::probe_read, dim3(ts::kProbeBlocks), dim3(256), st,
+               static_cast<const ts::u32x4 *>(src), bytes / 16, sink);
     return ts::check_launch("probe_read");
 }
 
@@ -61,11 +58,8 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream) 
     if (bytes == 0 || bytes % 16 != 0) return TS_ERR_SHAPE;
     if (!ts::aligned16(src) || !ts::aligned16(dst)) return TS_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    {
-        ts::ProfScope ps("probe_copy", st);
-        hipLaunchKernelGGL(ts::probe_copy, dim3(ts::kProbeBlocks), dim3(256), 0, st,
-                           static_cast<const ts::u32x4 *>(src), static_cast<ts::u32x4 *>(dst), bytes / 16);
-    }
+    ts::launch("probe_copy", ts::probe_copy, dim3(ts::kProbeBlocks), dim3(256), st,
+               static_cast<const ts::u32x4 *>(src), static_cast<ts::u32x4 *>(dst), bytes / 16);
     return ts::check_launch("probe_copy");
 }
 

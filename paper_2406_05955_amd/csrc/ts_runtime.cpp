@@ -47,6 +47,20 @@ ts_status check_launch(const char *where) {
     return TS_OK;
 }
 
+bool prof_events(const char *kernel, hipEvent_t *start, hipEvent_t *stop) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return false;
+    ProfRecord r;
+    r.kernel = kernel;
+    r.start = take_event();
+    r.stop = take_event();
+    if (!r.start || !r.stop) return false;
+    g_prof.push_back(r);
+    *start = r.start;
+    *stop = r.stop;
+    return true;
+}
+
 ProfScope::ProfScope(const char *kernel, hipStream_t stream) : stream_(stream) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof_on) return;
