@@ -30,8 +30,10 @@
 //   their W_down_t slices into a partial row per chunk.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
+#include "ts_batch.h"
 #include "ts_device.h"
 #include "ts_plan.h"
 #include "ts_runtime.h"
@@ -1098,7 +1100,7 @@ ts_status check_ffn_args(const float *x, const void *wg, const void *wu, const v
     s = check_stats(stats);
     if (s != TS_OK) return s;
     if (!plan_slots(hidden, inter, dt, batch, 1, plan)) return TS_ERR_SHAPE;
-    if (!ws || ws_bytes < plan->total) return TS_ERR_WORKSPACE;
+    if (!ws || ws_bytes < ffn_ws_bytes(batch, hidden, inter, dt)) return TS_ERR_WORKSPACE;
     if (!aligned16(ws)) return TS_ERR_ALIGN;
     return TS_OK;
 }
@@ -1117,7 +1119,7 @@ ts_status check_moe_args(const float *x, const void *wr, const void *wg, const v
     if (s != TS_OK) return s;
     if (stats && stats->n_union) return TS_ERR_UNSUPPORTED;
     if (!plan_slots(hidden, inter, dt, batch * K, K, plan)) return TS_ERR_SHAPE;
-    if (!ws || ws_bytes < plan->total) return TS_ERR_WORKSPACE;
+    if (!ws || ws_bytes < moe_ws_bytes(batch, hidden, inter, E, K, dt)) return TS_ERR_WORKSPACE;
     if (!aligned16(ws)) return TS_ERR_ALIGN;
     return TS_OK;
 }
@@ -1130,8 +1132,9 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
                                  ws, ws_bytes, &p);
     if (s != TS_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    int32_t *ridx = ws_at<int32_t>(ws, p.off_route_idx);
-    float *rw = ws_at<float>(ws, p.off_route_w);
+    const size_t roff = moe_route_offset(batch, hidden, inter, E, K, dt);
+    int32_t *ridx = ws_at<int32_t>(ws, roff);
+    float *rw = ws_at<float>(ws, roff + align_up256((size_t)batch * K * sizeof(int32_t)));
     if (dt == TS_F32)
         launch("moe_router", moe_router<float>, dim3((unsigned)batch), dim3(256), st, x,
                static_cast<const float *>(wr), hidden, E, K, ridx, rw);
@@ -1140,7 +1143,12 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
                static_cast<const uint16_t *>(wr), hidden, E, K, ridx, rw);
     s = check_launch("moe_router");
     if (s != TS_OK) return s;
-    s = run_slots(x, wg, wu, wd, ridx, (size_t)inter * (size_t)hidden, dt, dense, p, out, rw, stats, ws, st);
+    BatchPlan bp;
+    const size_t estride = (size_t)inter * (size_t)hidden;
+    if (!dense && batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp))
+        s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st);
+    else
+        s = run_slots(x, wg, wu, wd, ridx, estride, dt, dense, p, out, rw, stats, ws, st);
     if (s != TS_OK) return s;
     if (topk_idx) {
         if (hipMemcpyAsync(topk_idx, ridx, (size_t)batch * K * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
@@ -1166,8 +1174,23 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
     ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws,
                                      ws_bytes, &p);
     if (s != TS_OK) return s;
-    return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, false, p, out, nullptr, stats, ws,
-                         static_cast<hipStream_t>(stream));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // Several tokens with bf16 weights: the batched matrix-core path, in
+    // passes of up to 64 tokens (the union count needs a single pass).
+    const bool one_pass = batch <= ts::kBxMaxTokens;
+    if (batch > 1 && wdtype == TS_BF16 && ts::tuned("batch_path") == 0 &&
+        (one_pass || !(stats && stats->n_union))) {
+        for (int t0 = 0; t0 < batch; t0 += ts::kBxMaxTokens) {
+            const int nb = std::min(ts::kBxMaxTokens, batch - t0);
+            ts::BatchPlan bp;
+            if (!ts::plan_batch(nb, hidden, inter, 1, 1, wdtype, &bp)) return TS_ERR_SHAPE;
+            s = ts::run_batch(x + (size_t)t0 * hidden, w_gate, w_up, w_down_t, 0, nullptr, nullptr, bp,
+                              out + (size_t)t0 * hidden, stats, t0, ws, st);
+            if (s != TS_OK) return s;
+        }
+        return TS_OK;
+    }
+    return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, false, p, out, nullptr, stats, ws, st);
 }
 
 ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, const void *w_down_t, ts_dtype wdtype,

@@ -13,6 +13,7 @@ std::atomic<int> g_gate_tile{0};
 std::atomic<int> g_down_chunks{0};
 std::atomic<int> g_path{0};
 std::atomic<int> g_rif{0};
+std::atomic<int> g_batch{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
@@ -20,12 +21,15 @@ int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
 
 int tuned_tile() { return g_tile.load(); }
 
+size_t align_up256(size_t v) { return align256(v); }
+
 int tuned(const char *key) {
     if (std::strcmp(key, "ffn_tile") == 0) return g_tile.load();
     if (std::strcmp(key, "gate_tile") == 0) return g_gate_tile.load();
     if (std::strcmp(key, "down_chunks") == 0) return g_down_chunks.load();
     if (std::strcmp(key, "ffn_path") == 0) return g_path.load();
     if (std::strcmp(key, "rif") == 0) return g_rif.load();
+    if (std::strcmp(key, "batch_path") == 0) return g_batch.load();
     return 0;
 }
 
@@ -144,31 +148,83 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     return true;
 }
 
-bool plan_batch(int batch, int hidden, int inter, ts_dtype dt, BatchPlan *p) {
-    if (check_dims(batch, hidden, inter, dt) != TS_OK) return false;
+bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p) {
+    if (check_dims(batch, hidden, inter, dt) != TS_OK || dt != TS_BF16 || groups < 1 || top_k < 1) return false;
+    if (batch > kBxMaxTokens) return false;
     BatchPlan q;
     q.batch = batch;
     q.hidden = hidden;
     q.inter = inter;
-    q.esz = esize(dt);
-    q.bpad = batch <= 16 ? 16 : 32 * ((batch + 31) / 32);
-    q.total = 0;
+    q.groups = groups;
+    q.top_k = top_k;
+    // 16-token MFMA tiles: 1, 2 or 4 (the kernels are built for these)
+    q.nt = batch <= 16 ? 1 : (batch <= 32 ? 2 : 4);
+    q.bpad = 16 * q.nt;
+    q.hpad = (hidden + 63) / 64 * 64;
+    q.ntiles = (inter + kBxRows - 1) / kBxRows;
+    q.nslices = (hidden + kBxSliceCols - 1) / kBxSliceCols;
+    int want = g_down_chunks.load();
+    if (want <= 0) want = std::max(1, 512 / (q.nslices * groups));
+    q.nchunks = std::max(1, std::min(want, q.ntiles));
+    // a chunk's active rows (at most 32 per tile) must fit the LDS row list
+    q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, kDownMaxRows / kBxRows);
+    q.nchunks = (q.ntiles + q.tpc - 1) / q.tpc;
+    const size_t G = (size_t)groups, T = (size_t)q.ntiles;
+    size_t off = 0;
+    q.off_gcount = off;  // tokens per group
+    off = align256(off + G * sizeof(int32_t));
+    q.off_gtok = off;    // token of each (group, slot)
+    off = align256(off + G * q.bpad * sizeof(int32_t));
+    q.off_tslot = off;   // (group, slot) of each (token, routed rank)
+    off = align256(off + (size_t)batch * top_k * 2 * sizeof(int32_t));
+    q.off_xhl = off;     // x split into bf16 high and low parts: [G][2][bpad][hpad]
+    off = align256(off + G * 2 * q.bpad * q.hpad * sizeof(uint16_t));
+    q.off_cnt = off;     // per tile: |union G|, |union A|
+    off = align256(off + G * T * 2 * sizeof(int32_t));
+    q.off_aseg = off;    // per tile: union-active rows
+    off = align256(off + G * T * kBxRows * sizeof(int32_t));
+    q.off_hseg = off;    // per tile row: Combined for each token
+    off = align256(off + G * T * kBxRows * q.bpad * sizeof(float));
+    q.off_gmask = off;   // per tile and token: open-gate rows (bit mask)
+    off = align256(off + G * T * q.bpad * sizeof(uint32_t));
+    q.off_amask = off;   // per tile and token: active rows (bit mask)
+    off = align256(off + G * T * q.bpad * sizeof(uint32_t));
+    q.off_partial = off; // down partials: [G][bpad][nchunks][hidden]
+    off = align256(off + G * q.bpad * (size_t)q.nchunks * hidden * sizeof(float));
+    q.off_union = off;
+    off = align256(off + 4 * sizeof(int32_t));
+    q.total = off;
     *p = q;
     return true;
 }
 
+// Both the single-token and the batched plans must fit (the entry points
+// pick a path at call time, and the tuning knobs can move the choice).
 size_t ffn_ws_bytes(int batch, int hidden, int inter, ts_dtype dt) {
     if (check_dims(batch, hidden, inter, dt) != TS_OK) return 0;
     SlotPlan sp;
     if (!plan_slots(hidden, inter, dt, batch, 1, &sp)) return 0;
-    return sp.total;
+    size_t n = sp.total;
+    BatchPlan bp;
+    if (batch > 1 && plan_batch(std::min(batch, kBxMaxTokens), hidden, inter, 1, 1, dt, &bp))
+        n = std::max(n, bp.total);
+    return n;
+}
+
+size_t moe_route_offset(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt) {
+    SlotPlan sp;
+    if (!plan_slots(hidden, inter, dt, batch * top_k, top_k, &sp)) return 0;
+    size_t n = sp.total;
+    BatchPlan bp;
+    if (batch > 1 && plan_batch(batch, hidden, inter, n_experts, top_k, dt, &bp)) n = std::max(n, bp.total);
+    return align256(n);
 }
 
 size_t moe_ws_bytes(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt) {
     if (check_moe_dims(batch, hidden, inter, n_experts, top_k, dt) != TS_OK) return 0;
-    SlotPlan sp;
-    if (!plan_slots(hidden, inter, dt, batch * top_k, top_k, &sp)) return 0;
-    return sp.total;
+    // the router's outputs (expert ids, then weights) live past both plans
+    return moe_route_offset(batch, hidden, inter, n_experts, top_k, dt) +
+           2 * align256((size_t)batch * top_k * sizeof(int32_t));
 }
 
 }  // namespace ts
@@ -222,6 +278,11 @@ ts_status ts_tune_set(const char *key, int value) {
     if (std::strcmp(key, "rif") == 0) {
         if (value < 0 || value > 2) return TS_ERR_SHAPE;
         ts::g_rif.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "batch_path") == 0) {
+        if (value < 0 || value > 1) return TS_ERR_SHAPE;
+        ts::g_batch.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;

@@ -50,16 +50,27 @@ struct SlotPlan {
     size_t total = 0;
 };
 
-// Batched (batch > 1) FFN path: row unions and matrix-core contraction.
+// Batched path (bf16 weights, several tokens per weight set): every weight
+// row is read once per pass for up to kBxMaxTokens tokens, the contractions
+// run on the matrix cores.  A "group" is one weight set with its tokens: the
+// FFN has one group holding the batch, the MoE layer one group per expert
+// holding the tokens routed to it.
+constexpr int kBxMaxTokens = 64;  // tokens per group and pass
+constexpr int kBxRows = 32;       // neurons per gate+up wave tile
+constexpr int kBxSliceCols = 256; // output columns per down workgroup
+constexpr int kBxBlockRows = 32;  // down rows per MFMA K block
+
 struct BatchPlan {
-    int batch = 0, hidden = 0, inter = 0, esz = 0;
-    int bpad = 0;            // batch rounded up to the MFMA tile (16 or 32)
-    int gate_rows = 0;       // neurons per gate workgroup
-    int gate_blocks = 0;
-    int up_rows = 0;         // union rows per up workgroup
-    int down_split = 0;      // split of the union list in the down contraction
-    int down_cols = 0;       // output columns per down workgroup
-    size_t off_mask = 0, off_g = 0, off_cnt = 0, off_list = 0, off_h = 0, off_partial = 0, off_misc = 0;
+    int batch = 0, hidden = 0, inter = 0, groups = 1, top_k = 1;
+    int bpad = 0;        // tokens per group rounded up to 16 (MFMA N tile)
+    int nt = 0;          // 16-token tiles: bpad / 16
+    int hpad = 0;        // hidden rounded up to 64 (gate / up K blocks)
+    int ntiles = 0;      // 32-row wave tiles per group
+    int nslices = 0;     // 256-column slices of the down kernel
+    int nchunks = 0;     // tile chunks per group in the down kernel
+    int tpc = 0;         // tiles per chunk
+    size_t off_gcount = 0, off_gtok = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_aseg = 0, off_hseg = 0;
+    size_t off_gmask = 0, off_amask = 0, off_partial = 0, off_union = 0;
     size_t total = 0;
 };
 
@@ -67,7 +78,7 @@ int tuned_tile();
 int choose_tile(int inter);
 int tuned(const char *key);
 bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p);
-bool plan_batch(int batch, int hidden, int inter, ts_dtype dt, BatchPlan *p);
+bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p);
 
 ts_status check_dims(int batch, int hidden, int inter, ts_dtype dt);
 ts_status check_moe_dims(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt);
@@ -77,5 +88,7 @@ ts_status check_stats(const ts_ffn_stats *s);
 
 size_t ffn_ws_bytes(int batch, int hidden, int inter, ts_dtype dt);
 size_t moe_ws_bytes(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt);
+size_t moe_route_offset(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype dt);
+size_t align_up256(size_t v);
 
 }  // namespace ts

@@ -1,0 +1,140 @@
+"""Parity of the batched matrix-core path (ts_ffn_sparse / ts_moe_sparse with
+batch > 1 and bf16 weights) against the fp64 oracle, and against the
+single-token path (forced with the batch_path knob).
+
+Tolerance: relative L2 <= 1e-2 (bf16 weights, fp32 accumulation).  The
+batched path splits x and Combined into bf16 high / low parts, so its gate
+and up values carry about 2^-16 relative error per term; sets are compared
+outside |gate|, |up| < 1e-3."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import DEV, compare_sets, ffn_inputs_to_dev, list_of, rel_l2, to_dev
+from paper_2406_05955_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ts = pytest.importorskip("paper_2406_05955_amd.binding") if torch.cuda.is_available() else None
+
+THR = 1e-3
+
+
+def check_batch(inp, ref=None, union=True):
+    B, H, I = inp.shape
+    ref = ref or oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out, st = ts.ffn_sparse(x, wg, wu, wd, stats=True, union=union and B <= 64)
+    torch.cuda.synchronize()
+    err = rel_l2(out.cpu().numpy(), ref.y)
+    assert err <= 1e-2, (B, H, I, err)
+    for t in range(B):
+        g, u = ref.g[t], ref.u[t]
+        keep_g = np.abs(g) >= THR
+        keep_a = keep_g & (np.abs(u) >= THR)
+        assert compare_sets(list_of(st, "gate_idx", t, "n_gate"), g > 0, keep_g) == 0, t
+        assert compare_sets(list_of(st, "active_idx", t, "n_active"), (g > 0) & (u > 0), keep_a) == 0, t
+    if union and B <= 64:
+        ug = (ref.g > 0).any(axis=0)
+        ua = ((ref.g > 0) & (ref.u > 0)).any(axis=0)
+        near = ((np.abs(ref.g) < THR) | (np.abs(ref.u) < THR)).any(axis=0)
+        got = st["n_union"].cpu().tolist()
+        assert abs(got[0] - int(ug.sum())) <= int(near.sum()), (got, int(ug.sum()))
+        assert abs(got[1] - int(ua.sum())) <= int(near.sum()), (got, int(ua.sum()))
+    return out, st, ref
+
+
+@pytest.mark.parametrize("B,H,I", [(2, 512, 1000), (3, 200, 130), (8, 1024, 2048), (16, 64, 33), (17, 512, 700),
+                                   (32, 1000, 1500), (33, 256, 512), (64, 512, 1024), (65, 256, 300),
+                                   (130, 128, 96), (5, 8, 1), (4, 4096, 3001)])
+def test_batch_shapes(B, H, I):
+    inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=synth.BF16, seed=[31, B, H, I])
+    check_batch(inp)
+
+
+def test_batch_matches_single_token_path():
+    inp = synth.make_ffn(8, 2048, 4000, gate_bias=-0.84, dtype=synth.BF16, seed=32)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    a = ts.ffn_sparse(x, wg, wu, wd)
+    ts.tune_set("batch_path", 1)
+    try:
+        b = ts.ffn_sparse(x, wg, wu, wd)
+    finally:
+        ts.tune_set("batch_path", 0)
+    torch.cuda.synchronize()
+    assert rel_l2(a.cpu().numpy(), b.cpu().numpy().astype(np.float64)) <= 1e-3
+
+
+def test_batch_hot_cold_union():
+    """Skewed workload: a third of the neurons open often, the rest almost
+    never; per-token sparsity ~90%, union over 16 tokens ~67%."""
+    bias = synth.hot_cold_bias(3000, seed=5)
+    inp = synth.make_ffn(16, 1024, 3000, gate_bias=bias, dtype=synth.BF16, seed=33)
+    out, st, ref = check_batch(inp)
+    ua = int(((ref.g > 0) & (ref.u > 0)).any(axis=0).sum())
+    assert 0.2 * 3000 < ua < 0.45 * 3000
+
+
+@pytest.mark.parametrize("B", [8, 32])
+def test_mistral_shape_batch(B):
+    """hidden 4096, inter 14336, bf16, independent tokens at 90% sparsity each,
+    drawn on the device like the benchmark's layers; every output compared."""
+    L = synth.make_ffn_stack_torch(1, B, 4096, 14336, gate_bias=-0.8416, dtype=synth.BF16, seed=7, device=DEV)
+    inp = synth.FFNInputs(x=L["x"][0].cpu().numpy(), w_gate=synth.tensor_to_host_array(L["w_gate"][0], synth.BF16),
+                          w_up=synth.tensor_to_host_array(L["w_up"][0], synth.BF16),
+                          w_down_t=synth.tensor_to_host_array(L["w_down_t"][0], synth.BF16), dtype=synth.BF16,
+                          gate_bias=-0.8416)
+    check_batch(inp)
+
+
+def test_batch_deterministic():
+    inp = synth.make_ffn(24, 1024, 2000, gate_bias=-0.84, dtype=synth.BF16, seed=34)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    nbytes = ts.ffn_workspace_bytes(24, 1024, 2000, 1)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    ws.view(torch.float32)[: nbytes // 4].fill_(float("nan"))
+    a = ts.ffn_sparse(x, wg, wu, wd, ws=ws)
+    ws.view(torch.float32)[: nbytes // 4].fill_(float("nan"))
+    b = ts.ffn_sparse(x, wg, wu, wd, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(a).all().item()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def moe_check(m):
+    B, H, I, E, K = m.shape
+    ref = oracle.moe(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, m.dtype, K)
+    out, idx, w, st = ts.moe_sparse(to_dev(m.x), to_dev(m.w_router), to_dev(m.w_gate), to_dev(m.w_up),
+                                    to_dev(m.w_down_t), K, stats=True)
+    torch.cuda.synchronize()
+    p = np.sort(ref.probs, axis=1)[:, ::-1]
+    ties = [K < E and abs(p[t, K - 1] - p[t, K]) <= 1e-6 * p[t, K - 1] for t in range(B)]
+    keep = [t for t in range(B) if not ties[t]]
+    assert idx.cpu().numpy()[keep].tolist() == ref.topk_idx[keep].tolist()
+    assert rel_l2(out.cpu().numpy()[keep], ref.y[keep]) <= 1e-2
+    for t in keep:
+        for k in range(K):
+            s = t * K + k
+            g, u = ref.g[t, k], ref.u[t, k]
+            keep_a = (np.abs(g) >= THR) & (np.abs(u) >= THR)
+            n = int(st["n_active"][s])
+            assert compare_sets(st["active_idx"][s, :n].cpu().numpy(), (g > 0) & (u > 0), keep_a) == 0
+    return ref, out
+
+
+@pytest.mark.parametrize("B,H,I,E,K", [(16, 512, 700, 8, 2), (3, 256, 130, 4, 4), (2, 1024, 333, 1, 1),
+                                       (40, 256, 200, 64, 8), (16, 4096, 2048, 8, 2), (64, 128, 64, 3, 1)])
+def test_moe_batch_shapes(B, H, I, E, K):
+    m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=synth.BF16, seed=[35, B, H, I, E, K])
+    moe_check(m)
+
+
+def test_moe_batch_mixtral_shape():
+    L = synth.make_moe_stack_torch(1, 16, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=3,
+                                   device=DEV)
+    h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
+    m = synth.MoEInputs(x=L["x"][0].cpu().numpy(), w_router=h(L["w_router"][0]), w_gate=h(L["w_gate"][0]),
+                        w_up=h(L["w_up"][0]), w_down_t=h(L["w_down_t"][0]), dtype=synth.BF16, top_k=2,
+                        gate_bias=-1.5548)
+    moe_check(m)
