@@ -45,7 +45,7 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=32)
-    ap.add_argument("--workload", default="mistral", choices=["mistral", "sweep", "moe", "batch"])
+    ap.add_argument("--workload", default="mistral", choices=["mistral", "sweep", "moe", "batch", "all"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle CPU-baseline leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -265,6 +265,8 @@ def run_probes(ts, torch):
 
 
 def run_sweep(args, ts, synth, torch):
+    """Gate bias set for 50/75/90/95/99% zero Combined activations on the
+    Mistral-shaped stack, batch 1; dense comparator on every point."""
     out = []
     H, I, L = H_MISTRAL, I_MISTRAL, args.layers
     for s in (0.50, 0.75, 0.90, 0.95, 0.99):
@@ -280,11 +282,155 @@ def run_sweep(args, ts, synth, torch):
                     "measured_sparsity": 1 - sum(c[1] for c in counts) / (L * I),
                     "sparse_tokens_per_s_layer": L / ts_, "dense_tokens_per_s_layer": L / td,
                     "speedup": td / ts_, "byte_bound_speedup": dense / alg,
+                    "target_speedup_0.6x_byte_bound": 0.6 * dense / alg,
+                    "literal_target_0.6_over_1_minus_s": 0.6 / (1 - s),
                     "sparse_GBps_touched": alg / (ts_ / L) / 1e9, "dense_GBps": dense / (td / L) / 1e9,
                     "ffn_main_us": rl["avg_launch_us"], "ffn_main_GBps": rl["achieved"],
                     "ffn_reduce_us": rl["reduce"]["avg_launch_us"]})
         del stack
         torch.cuda.empty_cache()
+    return out
+
+
+def batch_kernels(ts, torch, fn, steps):
+    res = {}
+    for k in ("batch_dispatch", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
+        n, ms = kernel_avg_ms(ts, torch, fn, steps, k)
+        if n:
+            res[k + "_us"] = ms * 1e3
+    return res
+
+
+def run_batch_workload(args, ts, synth, torch):
+    """Mistral-shaped FFN stack with a batch of independent decode tokens
+    (batch 8 and 32): literal generator (each token ~90% sparse, union grows
+    with the batch) and the skewed hot/cold variant (union ~67% sparse)."""
+    import numpy as np
+    out = []
+    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
+    for B in (8, 32):
+        for variant in ("independent", "hot_cold"):
+            bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(I, seed=11)
+            stack = Stack(ts, synth, L, B, H, I, gate_bias=bias, seed=2)
+            counts = stack.counts()  # unions over the batch
+            t_s = timed(torch, stack.step_sparse, args.steps, args.warmup)
+            t_d = timed(torch, stack.step_dense, args.steps, args.warmup)
+            alg = sum(2 * H * (I + ng + na) + 8 * B * H for ng, na in counts) / L
+            dense = 3 * 2 * H * I + 8 * B * H
+            kt = batch_kernels(ts, torch, stack.step_sparse, max(3, args.steps // 3))
+            out.append({"workload": f"mistral7b_ffn_stack_bf16_b{B}_{variant}", "batch": B, "layers": L,
+                        "union_gate_fraction": sum(c[0] for c in counts) / (L * I),
+                        "union_active_fraction": sum(c[1] for c in counts) / (L * I),
+                        "sparse_tokens_per_s_layer": B * L / t_s, "dense_tokens_per_s_layer": B * L / t_d,
+                        "speedup": t_d / t_s, "byte_bound_speedup": dense / alg,
+                        "sparse_GBps_touched": alg / (t_s / L) / 1e9, "dense_GBps": dense / (t_d / L) / 1e9,
+                        "us_per_layer": t_s / L * 1e6, **kt})
+            del stack
+            torch.cuda.empty_cache()
+    return out
+
+
+class MoEStack:
+    """Device-resident MoE layers (router + packed experts) and marshalled
+    C-ABI arguments."""
+
+    def __init__(self, ts, synth, layers, batch, hidden, inter, E, K, gate_bias, seed=0):
+        import torch
+        self.ts, self.torch = ts, torch
+        self.L, self.B, self.H, self.I, self.E, self.K = layers, batch, hidden, inter, E, K
+        self.d = synth.make_moe_stack_torch(layers, batch, hidden, inter, E, K, gate_bias=gate_bias,
+                                            dtype=synth.BF16, seed=seed, device="cuda")
+        self.out = torch.empty(layers, batch, hidden, dtype=torch.float32, device="cuda")
+        self.idx = torch.empty(layers, batch, K, dtype=torch.int32, device="cuda")
+        self.w = torch.empty(layers, batch, K, dtype=torch.float32, device="cuda")
+        self.wsb = ts.moe_workspace_bytes(batch, hidden, inter, E, K, ts.TS_BF16)
+        self.ws = torch.empty(self.wsb, dtype=torch.uint8, device="cuda")
+        self.stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        vp = ctypes.c_void_p
+        self.args = [(vp(self.d["x"][l].data_ptr()), vp(self.d["w_router"][l].data_ptr()),
+                      vp(self.d["w_gate"][l].data_ptr()), vp(self.d["w_up"][l].data_ptr()),
+                      vp(self.d["w_down_t"][l].data_ptr()), ts.TS_BF16, batch, hidden, inter, E, K,
+                      vp(self.out[l].data_ptr()), vp(self.idx[l].data_ptr()), vp(self.w[l].data_ptr()))
+                     for l in range(layers)]
+
+    def step_sparse(self):
+        f = self.ts.lib.ts_moe_sparse
+        for a in self.args:
+            rc = f(*a, None, self.ws.data_ptr(), self.wsb, self.stream)
+            if rc:
+                raise RuntimeError(f"ts_moe_sparse -> {rc}")
+
+    def step_dense(self):
+        f = self.ts.lib.ts_moe_dense
+        for a in self.args:
+            rc = f(*a, self.ws.data_ptr(), self.wsb, self.stream)
+            if rc:
+                raise RuntimeError(f"ts_moe_dense -> {rc}")
+
+    def touched(self):
+        """Per layer: algorithmic bytes of the sparse MoE (router, and for each
+        expert hit its whole W_gate plus the union rows of W_up / W_down_t
+        over the tokens routed to it) and of the dense-routed comparator."""
+        import numpy as np
+        sp, dn = [], []
+        H, I, B, K = self.H, self.I, self.B, self.K
+        for l in range(self.L):
+            d = self.d
+            _, idx, _, st = self.ts.moe_sparse(d["x"][l], d["w_router"][l], d["w_gate"][l], d["w_up"][l],
+                                               d["w_down_t"][l], K, stats=True)
+            self.torch.cuda.synchronize()
+            idx = idx.cpu().numpy()
+            ng, na = st["n_gate"].cpu().numpy(), st["n_active"].cpu().numpy()
+            gi, ai = st["gate_idx"].cpu().numpy(), st["active_idx"].cpu().numpy()
+            b = 2 * self.E * H + 8 * B * H
+            bd = b
+            for e in np.unique(idx):
+                gsets, asets = [], []
+                for t in range(B):
+                    for k in range(K):
+                        if idx[t, k] == e:
+                            s = t * K + k
+                            gsets.append(gi[s, :ng[s]])
+                            asets.append(ai[s, :na[s]])
+                ug = len(np.unique(np.concatenate(gsets))) if gsets else 0
+                ua = len(np.unique(np.concatenate(asets))) if asets else 0
+                b += 2 * H * (I + ug + ua)
+                bd += 3 * 2 * H * I
+            sp.append(b)
+            dn.append(bd)
+        return sp, dn
+
+
+def run_moe_workload(args, ts, synth, torch):
+    """Mixtral-shaped MoE layer: 8 experts (hidden 4096, inter 14336, bf16),
+    top-2 softmax router, gate bias for 97% zero Combined activations inside
+    each expert (also the paper's 85% point), batch 1 and 16; 8 layers so a
+    step streams several GB."""
+    out = []
+    H, I, E, K, L = H_MISTRAL, I_MISTRAL, 8, 2, 8
+    for B in (1, 16):
+        for sp_target, bias in ((0.97, -1.5548), (0.85, -0.5244)):
+            if B == 16 and sp_target == 0.85:
+                continue
+            stack = MoEStack(ts, synth, L, B, H, I, E, K, gate_bias=bias, seed=4)
+            sp, dn = stack.touched()
+            t_s = timed(torch, stack.step_sparse, args.steps, args.warmup)
+            t_d = timed(torch, stack.step_dense, args.steps, args.warmup)
+            alg, dense = sum(sp) / L, sum(dn) / L
+            res = {"workload": f"mixtral_moe_bf16_b{B}_s{int(sp_target * 100)}", "batch": B, "layers": L,
+                   "experts": E, "top_k": K, "sparse_tokens_per_s_layer": B * L / t_s,
+                   "dense_tokens_per_s_layer": B * L / t_d, "speedup": t_d / t_s, "byte_bound_speedup": dense / alg,
+                   "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t_s / L) / 1e9,
+                   "dense_GBps": dense / (t_d / L) / 1e9, "us_per_layer": t_s / L * 1e6}
+            if B == 1:
+                for k in ("moe_router", "ffn_main", "ffn_reduce"):
+                    n, ms = kernel_avg_ms(ts, torch, stack.step_sparse, max(3, args.steps // 3), k)
+                    res[k + "_us"] = ms * 1e3
+            else:
+                res.update(batch_kernels(ts, torch, stack.step_sparse, max(3, args.steps // 3)))
+            out.append(res)
+            del stack
+            torch.cuda.empty_cache()
     return out
 
 
@@ -301,12 +447,12 @@ def main():
         ts.tune_set("ffn_tile", args.tile)
     if args.workload == "mistral":
         print(json.dumps(run_mistral(args, ts, synth, torch)), flush=True)
-    elif args.workload == "sweep":
-        for r in run_sweep(args, ts, synth, torch):
+        return
+    runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload}
+    names = list(runs) if args.workload == "all" else [args.workload]
+    for n in names:
+        for r in runs[n](args, ts, synth, torch):
             print(json.dumps(r), flush=True)
-    else:
-        print(json.dumps({"error": f"workload {args.workload} not built yet"}), flush=True)
-        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -44,8 +44,8 @@
  *   - Constraints: 1 <= batch <= 256; inter >= 1; hidden >= 8 and
  *     hidden % 8 == 0 (TS_BF16) or hidden % 4 == 0 (TS_F32); hidden <= 8192
  *     (TS_BF16) or <= 4096 (TS_F32); 1 <= n_experts <= 64;
- *     1 <= top_k <= min(n_experts, 8); x, weights, out, topk_w, topk_idx
- *     and ws 16-byte aligned; stats arrays 4-byte aligned.
+ *     1 <= top_k <= min(n_experts, 8); x, weights, out and ws 16-byte
+ *     aligned; topk_idx, topk_w and the stats arrays 4-byte aligned.
  *   - Non-finite inputs give unspecified (but memory-safe) results.
  *   - No exceptions cross this interface.
  */
@@ -187,9 +187,12 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
 
 /*
  * Tuning knobs (process-wide; 0 restores the default).  Keys:
- *   "ffn_tile"   neurons per workgroup of the fused single-token kernel
- *                (4..64, multiple of 4)
- *   "ffn_path"   0 = fused single-token kernel, 1 = split gate+up / down
+ *   "ffn_tile"   neurons per workgroup of the single-token kernels (4..128,
+ *                multiple of 4; the fused kernel caps it at 64)
+ *   "ffn_path"   0 = pipelined single-token kernel, 1 = split gate+up /
+ *                down, 2 = fused single-token kernel
+ *   "batch_path" 0 = matrix-core batched path for batch > 1 (bf16),
+ *                1 = single-token kernels per token
  *   "gate_tile"  neurons per workgroup of the split path's gate+up kernel
  *                (4..64, multiple of 4)
  *   "down_chunks" tile groups per slot in the split path's down kernel

@@ -11,9 +11,10 @@ namespace ts {
 
 // One pass for up to kBxMaxTokens tokens (plan p).  x / out point at the
 // pass's first token; topk / topw are the MoE routing table of those tokens
-// (null for the FFN); stats arrays are indexed from stats_base.
+// (null for the FFN); stats arrays are indexed from stats_base.  dense: take
+// every row (the dense comparator).
 ts_status run_batch(const float *x, const void *wg, const void *wu, const void *wd, size_t expert_stride,
                     const int32_t *topk, const float *topw, const BatchPlan &p, float *out,
-                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st);
+                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st, bool dense);
 
 }  // namespace ts

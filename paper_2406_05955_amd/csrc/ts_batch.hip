@@ -27,6 +27,8 @@
 //   bx_reduce    sums the chunk partials in a fixed order, applies routing
 //                weights; deterministic
 //   bx_stats     optional activity report from the per-tile bit masks
+// With `dense` set every row joins both unions: the dense comparator, which
+// reads all three matrices once for the whole batch.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -76,6 +78,7 @@ struct BxArgs {
     float *partial;          // [G][bpad][nchunks][H]
     float *out;              // [tokens][H]
     int want_masks;
+    int dense;               // 1: every row is taken (the dense comparator)
 };
 
 // ---------------------------------------------------------------------------
@@ -305,7 +308,7 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
             rowbit[mt][i] = r;
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-                open[mt][nt][i] = r0 + r < a.I && acc[mt][nt][i] > 0.f;
+                open[mt][nt][i] = r0 + r < a.I && (a.dense || acc[mt][nt][i] > 0.f);
                 if (wave == 0) s_g[r][16 * nt + lm] = acc[mt][nt][i];
             }
         }
@@ -362,7 +365,7 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
                 const float gv = s_g[r][16 * nt + lm];
                 const float uv = uacc[mt][nt][i];
                 const bool on = j < nu && gv > 0.f && uv > 0.f;
-                act[mt][nt][i] = on;
+                act[mt][nt][i] = on || (a.dense && j < nu);
                 hv[mt][nt][i] = on ? gv * uv : 0.f;
             }
         }
@@ -679,8 +682,9 @@ void launch_nt(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
 // pass's tokens.  Stats arrays are indexed from stats_base.
 ts_status run_batch(const float *x, const void *wg, const void *wu, const void *wd, size_t expert_stride,
                     const int32_t *topk, const float *topw, const BatchPlan &p, float *out,
-                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st) {
+                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st, bool dense) {
     BxArgs a;
+    a.dense = dense ? 1 : 0;
     a.x = x;
     a.wg = wg;
     a.wu = wu;

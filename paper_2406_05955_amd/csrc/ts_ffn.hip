@@ -336,11 +336,11 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     constexpr int CE = WTraits<WT>::CE;
     constexpr int NCD = (NC * 64 + kThreads - 1) / kThreads;
 
-    __shared__ float s_g[kMaxTile];
-    __shared__ float s_h[kMaxTile];
-    __shared__ int s_on[kMaxTile];
-    __shared__ int s_al[kMaxTile];
-    __shared__ float s_av[kMaxTile];
+    __shared__ float s_g[kMaxPipeTile];
+    __shared__ float s_h[kMaxPipeTile];
+    __shared__ int s_on[kMaxPipeTile];
+    __shared__ int s_al[kMaxPipeTile];
+    __shared__ float s_av[kMaxPipeTile];
     __shared__ int s_n[2];
 
     const int tid = threadIdx.x;
@@ -392,21 +392,27 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
 
     // ---- ballots: open gates (report) and non-zero Combined activations ------
     if (wave == 0) {
-        const bool in = lane < nt;
-        const bool pg = in && s_g[lane] > 0.f;
-        const uint64_t mg = __ballot(pg);
-        if (pg && a.want_seg) a.gseg[pr * a.tile + lane_prefix(mg, lane)] = n0 + lane;
-        const bool pa = in && s_on[lane];
-        const uint64_t ma = __ballot(pa);
-        if (pa) {
-            const int pos = lane_prefix(ma, lane);
-            s_al[pos] = lane;
-            s_av[pos] = s_h[lane];
-            if (a.want_seg) a.aseg[pr * a.tile + pos] = n0 + lane;
+        int ng = 0, na0 = 0;
+        for (int h = 0; h < kMaxPipeTile / 64; ++h) {
+            const int r = lane + 64 * h;
+            const bool in = r < nt;
+            const bool pg = in && s_g[r] > 0.f;
+            const uint64_t mg = __ballot(pg);
+            if (pg && a.want_seg) a.gseg[pr * a.tile + ng + lane_prefix(mg, lane)] = n0 + r;
+            const bool pa = in && s_on[r];
+            const uint64_t ma = __ballot(pa);
+            if (pa) {
+                const int pos = na0 + lane_prefix(ma, lane);
+                s_al[pos] = r;
+                s_av[pos] = s_h[r];
+                if (a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r;
+            }
+            ng += __popcll(mg);
+            na0 += __popcll(ma);
         }
         if (lane == 0) {
-            s_n[0] = __popcll(mg);
-            s_n[1] = __popcll(ma);
+            s_n[0] = ng;
+            s_n[1] = na0;
         }
     }
     __syncthreads();
@@ -820,30 +826,37 @@ __global__ __launch_bounds__(256) void ffn_union_count(const int32_t *__restrict
     }
 }
 
-// Router of the MoE layer, one 256-thread block per token: logits = W_r x
-// (one wave per expert row), then softmax, top-k (strictly larger wins, so
-// the lower index wins exact ties) and renormalisation by thread 0.
-template <typename WT>
+// Router of the MoE layer, one 256-thread block per token: x in registers,
+// each wave dots two expert rows at a time (all loads in flight), then
+// thread 0 takes the softmax, the top-k (strictly larger wins, so the lower
+// index wins exact ties) and the renormalised weights.
+template <typename WT, int NC>
 __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, const WT *__restrict__ wr, int H,
                                                   int E, int K, int32_t *__restrict__ topk_idx,
                                                   float *__restrict__ topk_w) {
     constexpr int CE = WTraits<WT>::CE;
+    constexpr int R = NC >= 16 ? 1 : 2;
     __shared__ float s_l[kMaxExperts];
     const int t = blockIdx.x;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const float *xt = x + (size_t)t * H;
     const int nch = H / CE;
-    for (int e = wave; e < E; e += 4) {
-        const WT *row = wr + (size_t)e * H;
-        float d = 0.f;
-        for (int c = lane; c < nch; c += 64) {
-            float f[CE];
-            unpack<WT>(ld_cached(row + c * CE), f);
+    float xr[NC][CE];
+    load_x<WT, NC>(x + (size_t)t * H, lane, nch, xr);
+    for (int e = wave; e < E; e += 4 * R) {
+        const WT *rows[R];
+        bool valid[R];
 #pragma unroll
-            for (int q = 0; q < CE; ++q) d = fmaf(f[q], xt[c * CE + q], d);
+        for (int k = 0; k < R; ++k) {
+            valid[k] = e + 4 * k < E;
+            rows[k] = wr + (size_t)(valid[k] ? e + 4 * k : e) * H;
         }
-        d = wave_sum(d);
-        if (lane == 0) s_l[e] = d;
+        float d[R];
+        dot_rows<WT, NC, R>(rows, valid, xr, lane, nch, d);
+        if (lane == 0) {
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                if (valid[k]) s_l[e + 4 * k] = d[k];
+        }
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -914,13 +927,14 @@ void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs 
 // with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
 // The pipelined kernel keeps x, two gate rows and two up rows in registers;
 // with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
-// MR, the unrolled rows per wave, is the smallest of 2, 4, 8 covering the tile.
+// MR, the unrolled rows per wave, is the smallest of 2, 4, 8, 16 covering the tile.
 template <typename WT, int NC>
 void launch_pipe_mr(int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
     const int rows = (tile + kWaves - 1) / kWaves;
     if (rows <= 2) launch("ffn_main", ffn_pipe<WT, NC, 2>, grid, dim3(kThreads), st, a);
     else if (rows <= 4) launch("ffn_main", ffn_pipe<WT, NC, 4>, grid, dim3(kThreads), st, a);
-    else launch("ffn_main", ffn_pipe<WT, NC, 8>, grid, dim3(kThreads), st, a);
+    else if (rows <= 8) launch("ffn_main", ffn_pipe<WT, NC, 8>, grid, dim3(kThreads), st, a);
+    else launch("ffn_main", ffn_pipe<WT, NC, 16>, grid, dim3(kThreads), st, a);
 }
 
 template <typename WT>
@@ -955,6 +969,20 @@ ts_status launch_reduce(const float *partial, int rows, const SlotPlan &p, const
     dim3 grid((unsigned)((p.hidden / 4 + kRedCols4 - 1) / kRedCols4), (unsigned)p.outs);
     launch("ffn_reduce", ffn_reduce, grid, dim3(256), st, partial, rows, p.hidden, p.slots_per_out, slot_w, out);
     return check_launch("ffn_reduce");
+}
+
+template <typename WT>
+void launch_router(int nc, int batch, hipStream_t st, const float *x, const void *wr, int H, int E, int K,
+                   int32_t *ridx, float *rw) {
+    const WT *w = static_cast<const WT *>(wr);
+    const dim3 g((unsigned)batch), b(256);
+    switch (nc) {
+    case 1: launch("moe_router", moe_router<WT, 1>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    case 2: launch("moe_router", moe_router<WT, 2>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    case 4: launch("moe_router", moe_router<WT, 4>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    case 8: launch("moe_router", moe_router<WT, 8>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    default: launch("moe_router", moe_router<WT, 16>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    }
 }
 
 ts_status run_report(const SlotPlan &p, const int32_t *cnt, const int32_t *gseg, const int32_t *aseg, int ntiles,
@@ -1048,10 +1076,11 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     a.wd = wd;
     a.route = route;
     a.expert_stride = expert_stride;
+    const bool use_pipe = pipe && p.nc <= 8;
     a.H = p.hidden;
     a.I = p.inter;
-    a.tile = p.tile;
-    a.ntiles = p.ntiles;
+    a.tile = use_pipe ? p.tile : p.ftile;
+    a.ntiles = use_pipe ? p.ntiles : p.fntiles;
     a.slots_per_tok = p.slots_per_out;
     a.cnt = ws_at<int32_t>(ws, p.off_cnt);
     a.gseg = ws_at<int32_t>(ws, p.off_gseg);
@@ -1059,11 +1088,11 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     a.partial = ws_at<float>(ws, p.off_partial);
     a.want_seg = want_seg ? 1 : 0;
     {
-        dim3 grid((unsigned)(p.slots * p.ntiles));
+        dim3 grid((unsigned)(p.slots * a.ntiles));
         const int rif = rows_in_flight(p.nc);
-        if (pipe && p.nc <= 8) {
-            if (dt == TS_F32) launch_pipe<float>(p.nc, p.tile, grid, st, a);
-            else launch_pipe<uint16_t>(p.nc, p.tile, grid, st, a);
+        if (use_pipe) {
+            if (dt == TS_F32) launch_pipe<float>(p.nc, a.tile, grid, st, a);
+            else launch_pipe<uint16_t>(p.nc, a.tile, grid, st, a);
         } else if (dt == TS_F32) {
             if (dense) launch_fused_nc<float, true>(p.nc, rif, grid, st, a);
             else launch_fused_nc<float, false>(p.nc, rif, grid, st, a);
@@ -1074,9 +1103,9 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     }
     ts_status s = check_launch("ffn_main");
     if (s != TS_OK) return s;
-    s = launch_reduce(a.partial, p.ntiles, p, slot_w, out, st);
+    s = launch_reduce(a.partial, a.ntiles, p, slot_w, out, st);
     if (s != TS_OK) return s;
-    return run_report(p, a.cnt, a.gseg, a.aseg, p.ntiles, p.tile, stats, ws, st);
+    return run_report(p, a.cnt, a.gseg, a.aseg, a.ntiles, a.tile, stats, ws, st);
 }
 
 ts_status run_slots(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
@@ -1113,7 +1142,7 @@ ts_status check_moe_args(const float *x, const void *wr, const void *wg, const v
     if (s != TS_OK) return s;
     if (!x || !wr || !wg || !wu || !wd || !out) return TS_ERR_NULL;
     if (!aligned16(x) || !aligned16(wr) || !aligned16(wg) || !aligned16(wu) || !aligned16(wd) || !aligned16(out) ||
-        (topk_idx && !aligned16(topk_idx)) || (topk_w && !aligned16(topk_w)))
+        (topk_idx && !aligned4(topk_idx)) || (topk_w && !aligned4(topk_w)))
         return TS_ERR_ALIGN;
     s = check_stats(stats);
     if (s != TS_OK) return s;
@@ -1135,18 +1164,14 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
     const size_t roff = moe_route_offset(batch, hidden, inter, E, K, dt);
     int32_t *ridx = ws_at<int32_t>(ws, roff);
     float *rw = ws_at<float>(ws, roff + align_up256((size_t)batch * K * sizeof(int32_t)));
-    if (dt == TS_F32)
-        launch("moe_router", moe_router<float>, dim3((unsigned)batch), dim3(256), st, x,
-               static_cast<const float *>(wr), hidden, E, K, ridx, rw);
-    else
-        launch("moe_router", moe_router<uint16_t>, dim3((unsigned)batch), dim3(256), st, x,
-               static_cast<const uint16_t *>(wr), hidden, E, K, ridx, rw);
+    if (dt == TS_F32) launch_router<float>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
+    else launch_router<uint16_t>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
     s = check_launch("moe_router");
     if (s != TS_OK) return s;
     BatchPlan bp;
     const size_t estride = (size_t)inter * (size_t)hidden;
-    if (!dense && batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp))
-        s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st);
+    if (batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp))
+        s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st, dense);
     else
         s = run_slots(x, wg, wu, wd, ridx, estride, dt, dense, p, out, rw, stats, ws, st);
     if (s != TS_OK) return s;
@@ -1185,7 +1210,7 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
             ts::BatchPlan bp;
             if (!ts::plan_batch(nb, hidden, inter, 1, 1, wdtype, &bp)) return TS_ERR_SHAPE;
             s = ts::run_batch(x + (size_t)t0 * hidden, w_gate, w_up, w_down_t, 0, nullptr, nullptr, bp,
-                              out + (size_t)t0 * hidden, stats, t0, ws, st);
+                              out + (size_t)t0 * hidden, stats, t0, ws, st, false);
             if (s != TS_OK) return s;
         }
         return TS_OK;
@@ -1199,8 +1224,19 @@ ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, con
     ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, nullptr, ws,
                                      ws_bytes, &p);
     if (s != TS_OK) return s;
-    return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, true, p, out, nullptr, nullptr, ws,
-                         static_cast<hipStream_t>(stream));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (batch > 1 && wdtype == TS_BF16 && ts::tuned("batch_path") == 0) {
+        for (int t0 = 0; t0 < batch; t0 += ts::kBxMaxTokens) {
+            const int nb = std::min(ts::kBxMaxTokens, batch - t0);
+            ts::BatchPlan bp;
+            if (!ts::plan_batch(nb, hidden, inter, 1, 1, wdtype, &bp)) return TS_ERR_SHAPE;
+            s = ts::run_batch(x + (size_t)t0 * hidden, w_gate, w_up, w_down_t, 0, nullptr, nullptr, bp,
+                              out + (size_t)t0 * hidden, nullptr, t0, ws, st, true);
+            if (s != TS_OK) return s;
+        }
+        return TS_OK;
+    }
+    return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, true, p, out, nullptr, nullptr, ws, st);
 }
 
 ts_status ts_moe_sparse(const float *x, const void *w_router, const void *w_gate, const void *w_up,

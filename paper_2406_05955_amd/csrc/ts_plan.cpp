@@ -33,15 +33,15 @@ int tuned(const char *key) {
     return 0;
 }
 
-// Neurons per workgroup for the single-token kernel: enough workgroups to
-// give every compute unit one (256 on MI355X), rounded to a multiple of 8
-// rows, at most one wave-ballot (64) per tile.
-int choose_tile(int inter) {
+// Neurons per workgroup for the single-token kernels: enough workgroups for
+// one per compute unit over all slots (256 on MI355X), a multiple of 8 rows,
+// at most `cap` (64 fused, 128 pipelined).  The ffn_tile knob overrides.
+int choose_tile(int inter, int slots, int cap) {
     int t = tuned_tile();
-    if (t > 0) return t;
-    int per = (inter + kTargetTiles - 1) / kTargetTiles;
+    if (t > 0) return std::min(t, cap);
+    long long per = ((long long)inter * slots + kTargetTiles - 1) / kTargetTiles;
     per = (per + 7) / 8 * 8;
-    return std::min(kMaxTile, std::max(8, per));
+    return (int)std::min<long long>(cap, std::max<long long>(8, per));
 }
 
 ts_status check_dims(int batch, int hidden, int inter, ts_dtype dt) {
@@ -87,19 +87,23 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     int need = (q.nch + 63) / 64;
     q.nc = 1;
     while (q.nc < need) q.nc <<= 1;
-    q.tile = choose_tile(inter);
+    q.tile = choose_tile(inter, slots, kMaxPipeTile);
     q.ntiles = (inter + q.tile - 1) / q.tile;
+    q.ftile = choose_tile(inter, slots, kMaxTile);
+    q.fntiles = (inter + q.ftile - 1) / q.ftile;
     q.slots = slots;
     q.slots_per_out = slots_per_out;
     q.outs = slots / slots_per_out;
-    size_t nst = (size_t)slots * (size_t)q.ntiles;
+    // regions sized for whichever kernel runs (the fused one has more tiles)
+    const size_t nst = (size_t)slots * (size_t)std::max(q.ntiles, q.fntiles);
+    const size_t nseg = (size_t)slots * std::max((size_t)q.ntiles * q.tile, (size_t)q.fntiles * q.ftile);
     size_t off = 0;
     q.off_cnt = off;
     off = align256(off + nst * 2 * sizeof(int32_t));
     q.off_gseg = off;
-    off = align256(off + nst * (size_t)q.tile * sizeof(int32_t));
+    off = align256(off + nseg * sizeof(int32_t));
     q.off_aseg = off;
-    off = align256(off + nst * (size_t)q.tile * sizeof(int32_t));
+    off = align256(off + nseg * sizeof(int32_t));
     q.off_partial = off;
     off = align256(off + nst * (size_t)hidden * sizeof(float));
     q.off_route_idx = off;
@@ -256,7 +260,7 @@ size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, i
 ts_status ts_tune_set(const char *key, int value) {
     if (!key) return TS_ERR_NULL;
     if (std::strcmp(key, "ffn_tile") == 0) {
-        if (value != 0 && (value < 4 || value > ts::kMaxTile || value % 4 != 0)) return TS_ERR_SHAPE;
+        if (value != 0 && (value < 4 || value > ts::kMaxPipeTile || value % 4 != 0)) return TS_ERR_SHAPE;
         ts::g_tile.store(value);
         return TS_OK;
     }

@@ -15,7 +15,8 @@ constexpr int kMaxExperts = 64;
 constexpr int kMaxTopK = 8;
 constexpr int kWaves = 8;                 // waves per workgroup of the single-token kernel
 constexpr int kThreads = kWaves * 64;     // 512 threads
-constexpr int kMaxTile = 64;              // neurons per workgroup: one wave ballot covers the tile
+constexpr int kMaxTile = 64;              // neurons per workgroup of the fused / gate+up kernels (one ballot)
+constexpr int kMaxPipeTile = 128;         // neurons per workgroup of the pipelined kernel (two ballots)
 constexpr int kTargetTiles = 256;         // one workgroup per compute unit on MI355X
 constexpr int kGateWaves = 4;             // waves per workgroup of the gate+up kernel
 constexpr int kGateThreads = kGateWaves * 64;
@@ -32,8 +33,10 @@ struct SlotPlan {
     int ce = 0;        // weight elements per 16-byte chunk
     int nch = 0;       // 16-byte chunks per weight row
     int nc = 0;        // chunks per lane in the row dot products (power of two)
-    int tile = 0;      // neurons per workgroup
-    int ntiles = 0;    // workgroups per slot
+    int tile = 0;      // neurons per workgroup of the pipelined kernel
+    int ntiles = 0;    // its workgroups per slot
+    int ftile = 0;     // neurons per workgroup of the fused kernel
+    int fntiles = 0;   // its workgroups per slot
     int slots = 0;     // number of slots
     int outs = 0;      // output rows (slots / slots_per_out)
     int slots_per_out = 1;
@@ -75,7 +78,7 @@ struct BatchPlan {
 };
 
 int tuned_tile();
-int choose_tile(int inter);
+int choose_tile(int inter, int slots, int cap);
 int tuned(const char *key);
 bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p);
 bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p);

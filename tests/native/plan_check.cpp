@@ -1,6 +1,7 @@
 // Host-only check of the launch planner's invariants over a grid of shapes.
 // Built with g++ (sanitizers on) by tests/test_plan_cpu.py; prints "ok" or
 // the first violated invariant.
+#include <algorithm>
 #include <cstdio>
 
 #include "ts_plan.h"
@@ -17,6 +18,7 @@ int main() {
     const int Is[] = {1, 3, 7, 8, 9, 63, 64, 65, 130, 777, 1792, 3001, 14336, 28672, 100000};
     const int Ss[] = {1, 2, 3, 8, 16, 32, 64, 256, 512, 2048};
     const int tiles[] = {0, 4, 8, 12, 20, 64};
+    const int ftiles[] = {0, 8, 56, 100, 128};
     const int chunks[] = {0, 1, 7, 32, 4096};
     const ts_dtype dts[] = {TS_F32, TS_BF16};
     for (ts_dtype dt : dts)
@@ -25,6 +27,8 @@ int main() {
                 for (int S : Ss)
                     for (int gt : tiles)
                         for (int ch : chunks) {
+                            const int ft = ftiles[(gt + ch) % 5];
+                            if (ts_tune_set("ffn_tile", ft) != TS_OK) return fail("tune ffn_tile", 0, H, I, S);
                             if (ts_tune_set("gate_tile", gt) != TS_OK) return fail("tune gate_tile", 0, H, I, S);
                             if (ts_tune_set("down_chunks", ch) != TS_OK) return fail("tune down_chunks", 0, H, I, S);
                             SlotPlan p;
@@ -41,8 +45,18 @@ int main() {
                                 return fail("nchunks cover", 1, H, I, S);
                             if (p.nslices * 64 < p.nch || (p.nslices - 1) * 64 >= p.nch) return fail("nslices", 1, H, I, S);
                             if (p.nc * 64 < p.nch || p.nc > 16) return fail("nc", 1, H, I, S);
-                            if (p.tile < 8 || p.tile > kMaxTile) return fail("tile", 1, H, I, S);
+                            if (p.tile < 8 || p.tile > kMaxPipeTile) return fail("tile", 1, H, I, S);
                             if ((long long)p.ntiles * p.tile < I) return fail("ntiles", 1, H, I, S);
+                            if (p.ftile < 8 || p.ftile > kMaxTile) return fail("ftile", 1, H, I, S);
+                            if ((long long)p.fntiles * p.ftile < I) return fail("fntiles", 1, H, I, S);
+                            if (p.off_gseg - p.off_cnt < (size_t)S * std::max(p.ntiles, p.fntiles) * 8)
+                                return fail("cnt size", 1, H, I, S);
+                            if (p.off_aseg - p.off_gseg <
+                                (size_t)S * std::max((size_t)p.ntiles * p.tile, (size_t)p.fntiles * p.ftile) * 4)
+                                return fail("seg size", 1, H, I, S);
+                            if (p.off_route_idx - p.off_partial <
+                                (size_t)S * std::max(p.ntiles, p.fntiles) * (size_t)H * 4)
+                                return fail("partial size", 1, H, I, S);
                             // workspace regions ordered, aligned and inside total
                             size_t offs[] = {p.off_cnt, p.off_gseg, p.off_aseg, p.off_partial, p.off_route_idx,
                                              p.off_route_w, p.off_aux, p.off_gcnt, p.off_ggseg, p.off_gaseg,
@@ -57,6 +71,7 @@ int main() {
                         }
     ts_tune_set("gate_tile", 0);
     ts_tune_set("down_chunks", 0);
+    ts_tune_set("ffn_tile", 0);
     std::printf("ok\n");
     return 0;
 }

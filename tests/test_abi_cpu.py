@@ -91,7 +91,7 @@ def test_moe_checks():
     assert call(K=0) == SHAPE
     assert call(K=9, E=16) == SHAPE
     assert call(K=3, E=2) == SHAPE
-    assert call(idx=A + 4) == ALIGN
+    assert call(idx=A + 2) == ALIGN
     need = ts.moe_workspace_bytes(1, 4096, 14336, 8, 2, 1)
     assert need > 0
     assert call(wsb=need - 1) == WS
@@ -108,7 +108,7 @@ def test_probe_checks():
 
 def test_tune_checks():
     assert ts.lib.ts_tune_set(b"ffn_tile", 10) == SHAPE
-    assert ts.lib.ts_tune_set(b"ffn_tile", 72) == SHAPE
+    assert ts.lib.ts_tune_set(b"ffn_tile", 132) == SHAPE
     assert ts.lib.ts_tune_set(b"nope", 8) == SHAPE
     assert ts.lib.ts_tune_set(b"ffn_tile", 32) == OK
     small = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
