@@ -11,19 +11,25 @@
 //
 // A group is one weight set and the tokens routed to it: the FFN has one
 // group, the MoE layer one per expert (tokens listed on the device by
-// bx_dispatch, ascending).  Kernels:
+// bx_dispatch, ascending).  x and Combined enter the matrix cores as two bf16
+// parts (v = hi + lo to 16 significant bits), so the products keep fp32-level
+// accuracy; with at most 8 token slots both parts share one 16-column MFMA
+// tile (columns 0-7 high, 8-15 low) and are added at the end.  Kernels:
 //   bx_dispatch  routing table -> per-group token lists and slots
 //   bx_prep      x of each group's tokens split into bf16 high and low parts
-//                (x = hi + lo to 16 significant bits, so the bf16 products
-//                keep fp32-level accuracy)
-//   bx_gate_up   per 32-neuron tile (4 waves, each a quarter of the hidden
-//                dimension): gate MFMA for all tokens, union of open gates,
-//                up MFMA over the union rows only, Combined, union of
-//                non-zero Combined (the tile's active rows and their values)
-//   bx_down      per (tile chunk, 256-column slice): active W_down_t rows
-//                staged through LDS in transposed order (the neuron index is
-//                the contraction axis but the slow axis of the row-major
-//                matrix), MFMA with Combined as the other operand
+//   bx_gate_up   per 32-neuron tile, 4 waves each a quarter of the hidden
+//                dimension with its own pipelined loads (no barrier inside
+//                the K loop): gate for all tokens, union of open gates, up
+//                over the union rows only (gathered), Combined, the tile's
+//                active rows as 32 slots and their Combined values as MFMA
+//                operand fragments
+//   bx_down      per (tile chunk, 128-column slice): 4 waves split the
+//                chunk's non-empty tiles; each wave stages a tile's active
+//                W_down_t rows in its own LDS region (row-major, XOR-swizzled
+//                16-byte chunks) and reads them back column-wise as the MFMA
+//                operand (the neuron index is the contraction axis but the
+//                slow axis of the row-major matrix); the 4 waves' sums are
+//                added in a fixed order at the end
 //   bx_reduce    sums the chunk partials in a fixed order, applies routing
 //                weights; deterministic
 //   bx_stats     optional activity report from the per-tile bit masks
@@ -42,6 +48,7 @@
 namespace ts {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ f32x4 mfma_bf16(const u32x4 a, const u32x4 b, const f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
@@ -59,11 +66,22 @@ __device__ __forceinline__ void split_hi_lo(float x, uint32_t &hi, uint32_t &lo)
     lo = bf16_bits(x - __uint_as_float(hi << 16));
 }
 
+// Shape constants per token-slot count TOK (8, 16, 32, 64).
+template <int TOK>
+struct Bx {
+    static constexpr bool PACK = TOK == 8;          // high and low parts share one 16-column tile
+    static constexpr int NT = PACK ? 1 : TOK / 16;  // 16-token accumulator tiles
+    static constexpr int NX = PACK ? 1 : 2 * NT;    // operand fragments per 32-wide k-step (x or Combined)
+    static constexpr int KS = NX <= 2 ? 4 : 2;      // k-steps per batch of gate / up loads
+    static constexpr int D = 2;                     // gate / up batches in flight per wave
+    static constexpr int DD = 2;                    // down tiles in flight per wave
+};
+
 struct BxArgs {
     const float *x;          // [tokens][H] (already offset to the pass's first token)
     const void *wg, *wu, *wd;
     size_t expert_stride;    // elements per expert matrix (0: one weight set)
-    int B, H, I, G, K, bpad, nt, hpad, ntiles, nslices, nchunks, tpc;
+    int B, H, I, G, K, bpad, hpad, ntiles, nslices, nchunks, tpc;
     const int32_t *topk;     // [B][K] routed experts, or null (FFN)
     const float *topw;       // [B][K] routing weights, or null
     int32_t *gcount;         // [G]
@@ -71,8 +89,8 @@ struct BxArgs {
     int32_t *tslot;          // [B][K][2] (group, slot) of each routed token
     uint16_t *xhl;           // [G][2][bpad][hpad]
     int32_t *cnt;            // [G][ntiles][2] |union G|, |union A|
-    int32_t *aseg;           // [G][ntiles][32] union-active rows (global index)
-    float *hseg;             // [G][ntiles][32][bpad] Combined per token
+    uint8_t *arow;           // [G][ntiles][32] row within the tile of each active slot (slot 0's past |union A|)
+    uint16_t *hfrag;         // [G][ntiles][2][bpad][32] Combined per active slot, bf16 high / low
     uint32_t *gmask;         // [G][ntiles][bpad] open-gate rows of the tile per token
     uint32_t *amask;         // [G][ntiles][bpad] active rows of the tile per token
     float *partial;          // [G][bpad][nchunks][H]
@@ -139,51 +157,65 @@ __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// K loop of the gate / up contraction for MT 16-row m-tiles (rows given per
-// lane) and NT 16-token n-tiles, over 64-wide K blocks [kb0, kb1).  A K block
-// reads 128 contiguous bytes of each row: lane (lm, lq) takes 16 bytes at
-// 8*lq and at 32 + 8*lq, the x fragments use the same K positions, so each
-// MFMA pairs matching K indices.  Weight chunks past H re-read the row's last
-// chunk; x is zero there.
-template <int MT, int NT>
-__device__ __forceinline__ void bx_kloop(const uint16_t *const (&rows)[MT], int H, const uint16_t *__restrict__ xh,
-                                         const uint16_t *__restrict__ xl, int hpad, int kb0, int kb1, int lm, int lq,
-                                         f32x4 (&acc)[MT][NT]) {
-    constexpr int U = NT <= 2 ? 2 : 1;  // K blocks per batch of loads
-    for (int kb = kb0; kb < kb1; kb += U) {
-        u32x4 w[U][MT][2], bh[U][NT][2], bl[U][NT][2];
+// K loop of the gate / up contraction of one wave: MT 16-row m-tiles (row
+// pointer per lane: row lm of each m-tile) against the NX operand fragments
+// of x (pointer per lane: column lm of each fragment), over nbat batches of
+// KS k-steps starting at k-step ks0.  k-step s covers 64 contiguous bytes of
+// each row: lane (lm, lq) takes the 16 bytes at k = 32 s + 8 lq for both
+// operands, so each MFMA pairs matching K indices.  The loads of the next
+// D - 1 batches are in flight while a batch is contracted (registers used
+// as a ring, no copies).  Weight chunks past H re-read the row's last chunk;
+// x is zero there.
+template <int TOK, int MT>
+__device__ __forceinline__ void bx_kloop(const uint16_t *const (&wrow)[MT], int H,
+                                         const uint16_t *const (&xrow)[Bx<TOK>::NX], int ks0, int nbat, int lq,
+                                         f32x4 (&acc)[MT][Bx<TOK>::NT]) {
+    using S = Bx<TOK>;
+    constexpr int KS = S::KS, D = S::D, NX = S::NX;
+    u32x4 w[D][MT][KS], xv[D][NX][KS];
+    auto issue = [&](int d, int b) {
+        const int kb = (ks0 + b * KS) * 32 + 8 * lq;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int kk = (kb + u < kb1 ? kb + u : kb) * 64;
+        for (int s = 0; s < KS; ++s) {
+            const int k = kb + 32 * s;
+            const int kw = k < H ? k : H - 8;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int k = kk + 32 * h + 8 * lq;
-                const int kw = k < H ? k : H - 8;
+            for (int mt = 0; mt < MT; ++mt) w[d][mt][s] = ld_stream(wrow[mt] + kw);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) w[u][mt][h] = ld_stream(rows[mt] + kw);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    const size_t xo = (size_t)(16 * nt + lm) * hpad + k;
-                    bh[u][nt][h] = ld_cached(xh + xo);
-                    bl[u][nt][h] = ld_cached(xl + xo);
-                }
-            }
+            for (int f = 0; f < NX; ++f) xv[d][f][s] = ld_cached(xrow[f] + k);
         }
+    };
+    auto mma = [&](int d) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (kb + u < kb1) {
+        for (int s = 0; s < KS; ++s)
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
+            for (int f = 0; f < NX; ++f)
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt)
+                for (int mt = 0; mt < MT; ++mt) {
+                    f32x4 &c = acc[mt][S::PACK ? 0 : f >> 1];
+                    c = mfma_bf16(w[d][mt][s], xv[d][f][s], c);
+                }
+    };
+    // nbat is a positive multiple of D; the steady loop has no branch, so
+    // the waits before each batch's MFMAs leave the later batches in flight
+    // (the scheduling barriers keep each batch's loads together and in ring
+    // order, so a wait for one batch does not also wait for the next)
 #pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) {
-                            acc[mt][nt] = mfma_bf16(w[u][mt][h], bh[u][nt][h], acc[mt][nt]);
-                            acc[mt][nt] = mfma_bf16(w[u][mt][h], bl[u][nt][h], acc[mt][nt]);
-                        }
-            }
+    for (int d = 0; d < D; ++d) {
+        issue(d, d);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int it = 0; it + D < nbat; it += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            mma(d);
+            __builtin_amdgcn_sched_barrier(0);
+            issue(d, it + D + d);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
+#pragma unroll
+    for (int d = 0; d < D; ++d) mma(d);
 }
 
 // Sum the four waves' K-quarter accumulators (fixed order); every wave gets
@@ -202,6 +234,18 @@ __device__ __forceinline__ void bx_combine(f32x4 (&acc)[2][NT], f32x4 (*s_red)[2
             acc[mt][nt] = (s_red[0][mt][nt][lane] + s_red[1][mt][nt][lane]) +
                           (s_red[2][mt][nt][lane] + s_red[3][mt][nt][lane]);
     __syncthreads();
+}
+
+// With packed fragments, column lm holds the high-part sum of token lm & 7
+// (lm < 8) or its low-part sum (lm >= 8): add the partner column, so both
+// lanes of a pair end with the same total.
+template <int TOK>
+__device__ __forceinline__ void bx_pair_sum(f32x4 (&acc)[2][Bx<TOK>::NT]) {
+    if (!Bx<TOK>::PACK) return;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[mt][0][i] += dpp_f32<0x128>(acc[mt][0][i]);  // row_ror:8
 }
 
 // Bit j (j < 32) set where row j of the tile has pred true for some token:
@@ -226,7 +270,7 @@ __device__ __forceinline__ uint32_t bx_any_rows(const bool (&pred)[2][NT][4]) {
 // Per token (lane lm of n-tile nt) the 32-bit mask of rows with pred true,
 // rows mapped through rowbit (tile-local row of union index j).
 template <int NT>
-__device__ __forceinline__ void bx_token_masks(const bool (&pred)[2][NT][4], const int (&rowbit)[2][4], int lq,
+__device__ __forceinline__ void bx_token_masks(const bool (&pred)[2][NT][4], const int (&rowbit)[2][4],
                                                uint32_t (&tm)[NT]) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -240,23 +284,31 @@ __device__ __forceinline__ void bx_token_masks(const bool (&pred)[2][NT][4], con
         m |= (uint32_t)__shfl_xor((int)m, 32, 64);
         tm[nt] = m;
     }
-    (void)lq;
 }
 
+// Position of the n-th (from 0) set bit of m, by halving with population
+// counts; n < popcount(m) (otherwise some position in 0..31).
 __device__ __forceinline__ int nth_set_bit(uint32_t m, int n) {
-    for (int b = 0; b < 32; ++b) {
-        if ((m >> b) & 1u) {
-            if (n == 0) return b;
-            --n;
+    int pos = 0;
+#pragma unroll
+    for (int w = 16; w >= 1; w >>= 1) {
+        const int c = __popc(m & ((1u << w) - 1u));
+        if (n >= c) {
+            n -= c;
+            m >>= w;
+            pos += w;
         }
     }
-    return 0;
+    return pos;
 }
 
-template <int NT>
+template <int TOK>
 __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
+    using S = Bx<TOK>;
+    constexpr int NT = S::NT, NX = S::NX;
     __shared__ f32x4 s_red[4][2][NT][64];
-    __shared__ float s_g[kBxRows][NT * 16];
+    __shared__ float s_g[kBxRows][TOK];
+    __shared__ __attribute__((aligned(16))) uint16_t s_h[2 * TOK][kBxRows];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
@@ -270,19 +322,28 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
             a.cnt[tix * 2 + 1] = 0;
         }
         if (a.want_masks)
-            for (int s = tid; s < a.bpad; s += 256) {
-                a.gmask[tix * a.bpad + s] = 0;
-                a.amask[tix * a.bpad + s] = 0;
+            for (int s = tid; s < TOK; s += 256) {
+                a.gmask[tix * TOK + s] = 0;
+                a.amask[tix * TOK + s] = 0;
             }
         return;
     }
+    for (int e = tid; e < 2 * TOK * kBxRows / 8; e += 256)
+        reinterpret_cast<u32x4 *>(&s_h[0][0])[e] = u32x4{0u, 0u, 0u, 0u};
+
     const int r0 = tile * kBxRows;
     const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)g * a.expert_stride;
     const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)g * a.expert_stride;
-    const uint16_t *xh = a.xhl + (size_t)(g * 2) * a.bpad * a.hpad;
-    const uint16_t *xl = a.xhl + (size_t)(g * 2 + 1) * a.bpad * a.hpad;
-    const int nkb = a.hpad / 64;
-    const int kb0 = wave * nkb / 4, kb1 = (wave + 1) * nkb / 4;
+    const uint16_t *xrow[NX];
+#pragma unroll
+    for (int f = 0; f < NX; ++f) {
+        const size_t r = S::PACK ? (size_t)g * 16 + lm : ((size_t)(g * 2 + (f & 1)) * TOK + 16 * (f >> 1) + lm);
+        xrow[f] = a.xhl + r * a.hpad;
+    }
+    const int kpw = a.hpad / 128;  // k-steps per wave (hpad / 32 over 4 waves)
+    const int ks0 = wave * kpw, nbat = kpw / S::KS;
+    // token of this lane's accumulator column, and whether the lane reports it
+    const bool tok_lane = !S::PACK || lm < 8;
 
     // ---- gate: 32 rows x all tokens --------------------------------------
     f32x4 acc[2][NT];
@@ -294,9 +355,10 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
         const uint16_t *rows[2];
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) rows[mt] = wg + (size_t)min(r0 + 16 * mt + lm, a.I - 1) * a.H;
-        bx_kloop<2, NT>(rows, a.H, xh, xl, a.hpad, kb0, kb1, lm, lq, acc);
+        bx_kloop<TOK, 2>(rows, a.H, xrow, ks0, nbat, lq, acc);
     }
     bx_combine<NT>(acc, s_red, wave, lane);
+    bx_pair_sum<TOK>(acc);
 
     bool open[2][NT][4];
     int rowbit[2][4];
@@ -309,17 +371,17 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 open[mt][nt][i] = r0 + r < a.I && (a.dense || acc[mt][nt][i] > 0.f);
-                if (wave == 0) s_g[r][16 * nt + lm] = acc[mt][nt][i];
+                if (wave == 0 && tok_lane) s_g[r][S::PACK ? lm : 16 * nt + lm] = acc[mt][nt][i];
             }
         }
     const uint32_t umask = bx_any_rows<NT>(open);
     const int nu = __popc(umask);
     if (a.want_masks) {
         uint32_t tm[NT];
-        bx_token_masks<NT>(open, rowbit, lq, tm);
-        if (wave == 0 && lq == 0)
+        bx_token_masks<NT>(open, rowbit, tm);
+        if (wave == 0 && lq == 0 && tok_lane)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) a.gmask[tix * a.bpad + 16 * nt + lm] = tm[nt];
+            for (int nt = 0; nt < NT; ++nt) a.gmask[tix * TOK + (S::PACK ? lm : 16 * nt + lm)] = tm[nt];
     }
     __syncthreads();  // s_g complete
 
@@ -329,27 +391,27 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) uacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int urow[2];  // tile-local row of union index 16*mt + lm (lanes past nu repeat the first)
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-        const int j = 16 * mt + lm;
-        urow[mt] = nth_set_bit(umask, j < nu ? j : 0);
-    }
     if (nu > 16) {
-        const uint16_t *rows[2] = {wu + (size_t)(r0 + urow[0]) * a.H, wu + (size_t)(r0 + urow[1]) * a.H};
-        bx_kloop<2, NT>(rows, a.H, xh, xl, a.hpad, kb0, kb1, lm, lq, uacc);
+        const uint16_t *rows[2];
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            const int j = 16 * mt + lm;
+            rows[mt] = wu + (size_t)(r0 + nth_set_bit(umask, j < nu ? j : 0)) * a.H;
+        }
+        bx_kloop<TOK, 2>(rows, a.H, xrow, ks0, nbat, lq, uacc);
     } else if (nu > 0) {
-        const uint16_t *rows[1] = {wu + (size_t)(r0 + urow[0]) * a.H};
+        const uint16_t *rows[1] = {wu + (size_t)(r0 + nth_set_bit(umask, lm < nu ? lm : 0)) * a.H};
         f32x4 u1[1][NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) u1[0][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        bx_kloop<1, NT>(rows, a.H, xh, xl, a.hpad, kb0, kb1, lm, lq, u1);
+        bx_kloop<TOK, 1>(rows, a.H, xrow, ks0, nbat, lq, u1);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) uacc[0][nt] = u1[0][nt];
     }
     bx_combine<NT>(uacc, s_red, wave, lane);
+    bx_pair_sum<TOK>(uacc);
 
-    // ---- Combined for union index j = 16*mt + 4*lq + i, token 16*nt + lm ----
+    // ---- Combined for union index j = 16*mt + 4*lq + i -------------------
     bool act[2][NT][4];
     float hv[2][NT][4];
     int ubit[2][4];
@@ -362,7 +424,7 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
             ubit[mt][i] = r;
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-                const float gv = s_g[r][16 * nt + lm];
+                const float gv = s_g[r][S::PACK ? (lm & 7) : 16 * nt + lm];
                 const float uv = uacc[mt][nt][i];
                 const bool on = j < nu && gv > 0.f && uv > 0.f;
                 act[mt][nt][i] = on || (a.dense && j < nu);
@@ -373,25 +435,39 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
     const int na = __popc(amask_u);
     if (a.want_masks) {
         uint32_t tm[NT];
-        bx_token_masks<NT>(act, ubit, lq, tm);
-        if (wave == 0 && lq == 0)
+        bx_token_masks<NT>(act, ubit, tm);
+        if (wave == 0 && lq == 0 && tok_lane)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) a.amask[tix * a.bpad + 16 * nt + lm] = tm[nt];
+            for (int nt = 0; nt < NT; ++nt) a.amask[tix * TOK + (S::PACK ? lm : 16 * nt + lm)] = tm[nt];
     }
-    if (wave == 0) {
+    // active union index j -> slot (its rank); Combined into the fragment block
+    if (wave == 0 && tok_lane) {
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int j = 16 * mt + 4 * lq + i;
                 if ((amask_u >> j) & 1u) {
-                    const int rank = __popc(amask_u & ((1u << j) - 1u));
-                    float *hrow = a.hseg + (tix * kBxRows + rank) * a.bpad;
+                    const int slot = __popc(amask_u & ((1u << j) - 1u));
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) hrow[16 * nt + lm] = hv[mt][nt][i];
-                    if (lm == 0) a.aseg[tix * kBxRows + rank] = r0 + ubit[mt][i];
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const int t = S::PACK ? lm : 16 * nt + lm;
+                        uint32_t hi, lo;
+                        split_hi_lo(hv[mt][nt][i], hi, lo);
+                        s_h[t][slot] = (uint16_t)hi;
+                        s_h[TOK + t][slot] = (uint16_t)lo;
+                    }
                 }
             }
+    }
+    __syncthreads();  // s_h complete
+    u32x4 *hdst = reinterpret_cast<u32x4 *>(a.hfrag + tix * (2 * TOK * kBxRows));
+    for (int e = tid; e < 2 * TOK * kBxRows / 8; e += 256) hdst[e] = reinterpret_cast<const u32x4 *>(&s_h[0][0])[e];
+    if (wave == 0) {
+        if (lane < kBxRows) {  // an empty tile lists row 0 (always < I), never used
+            const int j = nth_set_bit(amask_u, lane < na ? lane : 0);
+            a.arow[tix * kBxRows + lane] = na > 0 ? (uint8_t)nth_set_bit(umask, j) : (uint8_t)0;
+        }
         if (lane == 0) {
             a.cnt[tix * 2] = nu;
             a.cnt[tix * 2 + 1] = na;
@@ -400,27 +476,28 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Down: workgroup (group, chunk of tiles, 256-column slice), 4 waves.  The
-// chunk's active rows are processed in K blocks of 32 rows: each block's
-// W_down_t[row][slice] (16 KB) and Combined[row][tokens] are loaded with
-// coalesced 16-byte loads, written to LDS transposed (column-major W,
-// token-major Combined split into bf16 high / low parts), and contracted:
-// wave w owns columns 64w..64w+63 (4 n-tiles), all token m-tiles.  The next
-// block's loads are in flight while the current block is contracted.
+// Down: workgroup (group, chunk of tiles, 128-column slice), 4 waves; wave w
+// takes every 4th non-empty tile of the chunk.  A tile is one K block of 32
+// slots: its active W_down_t rows (slots past |union A| repeat slot 0's row,
+// with zero Combined) x the slice's 128 columns, 8 KB loaded as 8 coalesced
+// 16-byte loads per lane (lane (lq, lm): slot 4q + lq, columns 8 lm..8 lm+7)
+// and written to the wave's own LDS region row-major, the 16-byte chunk c
+// of slot s stored at position c ^ (2 ((s >> 3) & 3)).  The MFMA operand of
+// n-tile nc (columns 16 nc + lm) takes slots 8 lq .. 8 lq + 7 of one column:
+// eight 2-byte LDS reads whose 16 lanes of each lq hit 8 banks of their own
+// (the swizzle moves the four lq groups apart), so neither the writes nor
+// the reads conflict.  The other operand is the tile's Combined fragment
+// (token rows, slots contiguous) as written by bx_gate_up.  Loads of the
+// next DD - 1 tiles are in flight while a tile is contracted.
+template <int TOK>
+__global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
+    using S = Bx<TOK>;
+    constexpr int NT = S::NT, NX = S::NX, DD = S::DD;
+    constexpr int REG = 512 * NT;  // 16-byte units per wave: 8 KB staging, or its 8 x NT accumulators
+    constexpr int BG = 2;          // n-tiles whose operands are read from LDS together
+    __shared__ u32x4 s_lds[4 * REG];
 
-constexpr int kBxPadRows = kBxBlockRows + 8;  // LDS row stride in the transposed tiles
-
-template <int NT>
-__global__ __launch_bounds__(256) void bx_down(BxArgs a) {
-    constexpr int TOK = NT * 16;
-    constexpr int HQ = (kBxBlockRows * TOK / 4 + 255) / 256;  // Combined float4 per thread per block
-    __shared__ int s_row[kDownMaxRows];
-    __shared__ int s_hidx[kDownMaxRows];
-    __shared__ int s_cnt[kDownMaxTiles + 1];
-    __shared__ uint16_t sW[2][kBxSliceCols][kBxPadRows];
-    __shared__ uint16_t sH[2][2][TOK][kBxPadRows];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lm = lane & 15, lq = lane >> 4;
     const int slice = blockIdx.x % a.nslices;
     const int chunk = (blockIdx.x / a.nslices) % a.nchunks;
@@ -432,131 +509,135 @@ __global__ __launch_bounds__(256) void bx_down(BxArgs a) {
     const int ntc = min(a.tpc, a.ntiles - t0);
     const size_t tbase = (size_t)g * a.ntiles + t0;
 
-    // 1. rows of the chunk (ascending tiles, ascending within a tile)
-    for (int t = tid; t < ntc; t += 256) s_cnt[t] = a.cnt[(tbase + t) * 2 + 1];
-    __syncthreads();
-    if (tid == 0) {
-        int off = 0;
-        for (int t = 0; t < ntc; ++t) {
-            const int c = s_cnt[t];
-            s_cnt[t] = off;
-            off += c;
-        }
-        s_cnt[ntc] = off;
+    // lane t: |union A| and slot rows of the chunk's tile t
+    int na_l = 0;
+    u32x4 rt0 = {0u, 0u, 0u, 0u}, rt1 = {0u, 0u, 0u, 0u};
+    if (lane < ntc) {
+        na_l = a.cnt[(tbase + lane) * 2 + 1];
+        rt0 = *reinterpret_cast<const u32x4 *>(a.arow + (tbase + lane) * kBxRows);
+        rt1 = *reinterpret_cast<const u32x4 *>(a.arow + (tbase + lane) * kBxRows + 16);
     }
-    __syncthreads();
-    for (int e = tid; e < ntc * kBxRows; e += 256) {
-        const int t = e / kBxRows, q = e % kBxRows;
-        if (q < s_cnt[t + 1] - s_cnt[t]) {
-            s_row[s_cnt[t] + q] = a.aseg[(tbase + t) * kBxRows + q];
-            s_hidx[s_cnt[t] + q] = (int)((tbase + t) * kBxRows + q);
-        }
-    }
-    __syncthreads();
-    const int nrows = s_cnt[ntc];
-    const int nblk = (nrows + kBxBlockRows - 1) / kBxBlockRows;
+    const uint64_t ne = __ballot(na_l > 0);
+    const bool mine = ((ne >> lane) & 1ull) && (lane_prefix(ne, lane) & 3) == wave;
+    uint64_t mq = __ballot(mine);  // this wave's tiles, taken lowest first
+    const int nblk = __popcll(mq);
 
     const uint16_t *wd = reinterpret_cast<const uint16_t *>(a.wd) + (size_t)g * a.expert_stride;
     const int col0 = slice * kBxSliceCols;
+    const int cw = min(col0 + 8 * lm, H - 8);
+    u32x4 *sw = s_lds + wave * REG;
+    const uint16_t *sw16 = reinterpret_cast<const uint16_t *>(sw);
 
-    // per-thread share of a block: 4 W chunks (row = item / 32, 8 columns at
-    // 8 * (item % 32)) and HQ Combined float4 (row = q / (TOK/4), tokens 4x)
-    u32x4 wv[4];
-    f32x4 hq[HQ];
-    auto load_block = [&](int blk) {
+    u32x4 wv[DD][8], hq[DD][NX];
+    // tiles are issued in order; with none left (prologue of a wave with
+    // fewer than DD tiles) tile 0 of the chunk is loaded and never used
+    auto issue = [&](int d) {
+        const int t = mq ? __builtin_ctzll(mq) : 0;
+        mq &= mq - 1ull;
+        const uint32_t tr[8] = {rt0.x, rt0.y, rt0.z, rt0.w, rt1.x, rt1.y, rt1.z, rt1.w};
+        const size_t rowbase = (size_t)(t0 + t) * kBxRows;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int item = tid + 256 * j;
-            const int r = blk * kBxBlockRows + item / 32;
-            const int row = s_row[r < nrows ? r : 0];
-            int c = col0 + 8 * (item % 32);
-            c = c < H ? c : H - 8;
-            wv[j] = ld_stream(wd + (size_t)row * H + c);
+        for (int q = 0; q < 8; ++q) {
+            const uint32_t wq = (uint32_t)__builtin_amdgcn_readlane((int)tr[q], t);
+            const int rr = (int)((wq >> (8 * lq)) & 0xFFu);
+            wv[d][q] = ld_stream(wd + (rowbase + rr) * H + cw);
         }
+        const uint16_t *hb = a.hfrag + (tbase + t) * (2 * TOK * kBxRows);
 #pragma unroll
-        for (int j = 0; j < HQ; ++j) {
-            const int q = tid + 256 * j;
-            const int rl = q / (TOK / 4);
-            const int r = blk * kBxBlockRows + rl;
-            const bool ok = rl < kBxBlockRows && r < nrows;
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(a.hseg + (size_t)s_hidx[ok ? r : 0] * a.bpad +
-                                                             4 * (q % (TOK / 4)));
-            hq[j] = ok ? v : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int f = 0; f < NX; ++f) {
+            const int fr = S::PACK ? lm : (f & 1) * TOK + 16 * (f >> 1) + lm;
+            hq[d][f] = ld_cached(hb + fr * kBxRows + 8 * lq);
         }
     };
-    auto store_block = [&](int buf) {
+
+    f32x4 acc[8][NT];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int item = tid + 256 * j;
-            const int rl = item / 32, cb = 8 * (item % 32);
-            const uint32_t w4[4] = {wv[j].x, wv[j].y, wv[j].z, wv[j].w};
+    for (int nc = 0; nc < 8; ++nc)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                sW[buf][cb + 2 * e][rl] = (uint16_t)(w4[e] & 0xFFFFu);
-                sW[buf][cb + 2 * e + 1][rl] = (uint16_t)(w4[e] >> 16);
-            }
+        for (int nt = 0; nt < NT; ++nt) acc[nc][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto mma = [&](int d) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int slot = 4 * q + lq;
+            sw[slot * 16 + (lm ^ (2 * ((slot >> 3) & 3)))] = wv[d][q];
         }
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int j = 0; j < HQ; ++j) {
-            const int q = tid + 256 * j;
-            const int rl = q / (TOK / 4);
-            if (rl < kBxBlockRows) {
-                const int tk = 4 * (q % (TOK / 4));
-                const float v4[4] = {hq[j].x, hq[j].y, hq[j].z, hq[j].w};
+        for (int n2 = 0; n2 < 8; n2 += BG) {
+            u16x8 bfr[BG];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t hi, lo;
-                    split_hi_lo(v4[e], hi, lo);
-                    sH[buf][0][tk + e][rl] = (uint16_t)hi;
-                    sH[buf][1][tk + e][rl] = (uint16_t)lo;
+            for (int u = 0; u < BG; ++u) {
+                const int pos = (2 * (n2 + u) + (lm >> 3)) ^ (2 * lq);
+                const uint16_t *src = sw16 + (8 * lq) * kBxSliceCols + 8 * pos + (lm & 7);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) bfr[u][j] = src[j * kBxSliceCols];
+            }
+#pragma unroll
+            for (int u = 0; u < BG; ++u) {
+                const u32x4 b = __builtin_bit_cast(u32x4, bfr[u]);
+#pragma unroll
+                for (int f = 0; f < NX; ++f) {
+                    f32x4 &c = acc[n2 + u][S::PACK ? 0 : f >> 1];
+                    c = mfma_bf16(hq[d][f], b, c);
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
+        __builtin_amdgcn_wave_barrier();
     };
 
-    f32x4 acc[NT][4];
+    // steady loop without branches (every issue is a real tile), then the
+    // last (fewer than 2 DD) tiles
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt)
+    for (int d = 0; d < DD; ++d) issue(d);
+    int b = 0;
+    for (; b + 2 * DD <= nblk; b += DD) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    if (nblk > 0) {
-        load_block(0);
-        store_block(0);
-    }
-    __syncthreads();
-    for (int blk = 0; blk < nblk; ++blk) {
-        const int buf = blk & 1;
-        if (blk + 1 < nblk) load_block(blk + 1);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = 64 * wave + 16 * j + lm;
-            const u32x4 bw = *reinterpret_cast<const u32x4 *>(&sW[buf][col][8 * lq]);
-#pragma unroll
-            for (int mt = 0; mt < NT; ++mt) {
-                const u32x4 ah = *reinterpret_cast<const u32x4 *>(&sH[buf][0][16 * mt + lm][8 * lq]);
-                const u32x4 al = *reinterpret_cast<const u32x4 *>(&sH[buf][1][16 * mt + lm][8 * lq]);
-                acc[mt][j] = mfma_bf16(ah, bw, acc[mt][j]);
-                acc[mt][j] = mfma_bf16(al, bw, acc[mt][j]);
-            }
+        for (int d = 0; d < DD; ++d) {
+            mma(d);
+            issue(d);
         }
-        if (blk + 1 < nblk) store_block(buf ^ 1);
-        __syncthreads();
     }
+#pragma unroll
+    for (int d = 0; d < DD; ++d) {
+        if (b + d < nblk) {
+            mma(d);
+            if (b + d + DD < nblk) issue(d);
+        }
+    }
+#pragma unroll
+    for (int d = 0; d < DD; ++d)
+        if (b + DD + d < nblk) mma(d);
 
-    // D[m = token 16*mt + 4*lq + i][n = column 64*wave + 16*j + lm]
+    // the four waves' sums, added in a fixed order; wave w finishes n-tiles 2w, 2w + 1
+    f32x4 *sa = reinterpret_cast<f32x4 *>(sw);
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt)
+    for (int nc = 0; nc < 8; ++nc)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = col0 + 64 * wave + 16 * j + lm;
+        for (int nt = 0; nt < NT; ++nt) sa[(nc * NT + nt) * 64 + lane] = acc[nc][nt];
+    __syncthreads();
+    const f32x4 *s0 = reinterpret_cast<const f32x4 *>(s_lds);
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+        const int nc = 2 * wave + k2;
+        const int col = col0 + 16 * nc + lm;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int e = (nc * NT + nt) * 64 + lane;
+            f32x4 v = (s0[e] + s0[REG + e]) + (s0[2 * REG + e] + s0[3 * REG + e]);
+            if (S::PACK) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] += __shfl_xor(v[i], 32, 64);
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int tok = 16 * mt + 4 * lq + i;
-                if (tok < ng && col < H)
-                    a.partial[(((size_t)g * a.bpad + tok) * a.nchunks + chunk) * H + col] = acc[mt][j][i];
+                const int tok = 16 * nt + 4 * lq + i;
+                const bool ok = (S::PACK ? lq < 2 : true) && tok < ng && col < H;
+                if (ok) a.partial[(((size_t)g * TOK + tok) * a.nchunks + chunk) * H + col] = v[i];
             }
         }
+    }
 }
 
 // out[t][:] = sum over routed ranks k (ascending) of w[t][k] times the sum
@@ -669,10 +750,10 @@ T *ws_at(void *ws, size_t off) {
     return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
 }
 
-template <int NT>
-void launch_nt(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
-    launch("batch_gate_up", bx_gate_up<NT>, dim3((unsigned)(p.groups * p.ntiles)), dim3(256), st, a);
-    launch("batch_down", bx_down<NT>, dim3((unsigned)(p.groups * p.nchunks * p.nslices)), dim3(256), st, a);
+template <int TOK>
+void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
+    launch("batch_gate_up", bx_gate_up<TOK>, dim3((unsigned)(p.groups * p.ntiles)), dim3(256), st, a);
+    launch("batch_down", bx_down<TOK>, dim3((unsigned)(p.groups * p.nchunks * p.nslices)), dim3(256), st, a);
 }
 
 }  // namespace
@@ -696,7 +777,6 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     a.G = p.groups;
     a.K = p.top_k;
     a.bpad = p.bpad;
-    a.nt = p.nt;
     a.hpad = p.hpad;
     a.ntiles = p.ntiles;
     a.nslices = p.nslices;
@@ -709,8 +789,8 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     a.tslot = ws_at<int32_t>(ws, p.off_tslot);
     a.xhl = ws_at<uint16_t>(ws, p.off_xhl);
     a.cnt = ws_at<int32_t>(ws, p.off_cnt);
-    a.aseg = ws_at<int32_t>(ws, p.off_aseg);
-    a.hseg = ws_at<float>(ws, p.off_hseg);
+    a.arow = ws_at<uint8_t>(ws, p.off_arow);
+    a.hfrag = ws_at<uint16_t>(ws, p.off_hfrag);
     a.gmask = ws_at<uint32_t>(ws, p.off_gmask);
     a.amask = ws_at<uint32_t>(ws, p.off_amask);
     a.partial = ws_at<float>(ws, p.off_partial);
@@ -720,10 +800,11 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
 
     launch("batch_dispatch", bx_dispatch, dim3(1), dim3(64), st, a);
     launch("batch_prep", bx_prep, dim3((unsigned)(p.groups * p.bpad)), dim3(256), st, a);
-    switch (p.nt) {
-    case 1: launch_nt<1>(p, a, st); break;
-    case 2: launch_nt<2>(p, a, st); break;
-    default: launch_nt<4>(p, a, st); break;
+    switch (p.tok) {
+    case 8: launch_tok<8>(p, a, st); break;
+    case 16: launch_tok<16>(p, a, st); break;
+    case 32: launch_tok<32>(p, a, st); break;
+    default: launch_tok<64>(p, a, st); break;
     }
     launch("batch_reduce", bx_reduce, dim3((unsigned)((p.hidden / 4 + 3) / 4), (unsigned)p.batch), dim3(256), st, a);
     ts_status s = check_launch("batch path");

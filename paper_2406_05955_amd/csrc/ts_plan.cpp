@@ -161,40 +161,39 @@ bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtyp
     q.inter = inter;
     q.groups = groups;
     q.top_k = top_k;
-    // 16-token MFMA tiles: 1, 2 or 4 (the kernels are built for these)
-    q.nt = batch <= 16 ? 1 : (batch <= 32 ? 2 : 4);
-    q.bpad = 16 * q.nt;
-    q.hpad = (hidden + 63) / 64 * 64;
+    // token slots per group: the kernels are built for 8, 16, 32 and 64
+    q.tok = batch <= 8 ? 8 : (batch <= 16 ? 16 : (batch <= 32 ? 32 : 64));
+    q.bpad = q.tok;
+    q.hpad = (hidden + kBxKQuant - 1) / kBxKQuant * kBxKQuant;
     q.ntiles = (inter + kBxRows - 1) / kBxRows;
     q.nslices = (hidden + kBxSliceCols - 1) / kBxSliceCols;
     int want = g_down_chunks.load();
     if (want <= 0) want = std::max(1, 512 / (q.nslices * groups));
     q.nchunks = std::max(1, std::min(want, q.ntiles));
-    // a chunk's active rows (at most 32 per tile) must fit the LDS row list
-    q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, kDownMaxRows / kBxRows);
+    q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, kBxChunkTiles);
     q.nchunks = (q.ntiles + q.tpc - 1) / q.tpc;
     const size_t G = (size_t)groups, T = (size_t)q.ntiles;
     size_t off = 0;
     q.off_gcount = off;  // tokens per group
     off = align256(off + G * sizeof(int32_t));
     q.off_gtok = off;    // token of each (group, slot)
-    off = align256(off + G * q.bpad * sizeof(int32_t));
+    off = align256(off + G * q.tok * sizeof(int32_t));
     q.off_tslot = off;   // (group, slot) of each (token, routed rank)
     off = align256(off + (size_t)batch * top_k * 2 * sizeof(int32_t));
-    q.off_xhl = off;     // x split into bf16 high and low parts: [G][2][bpad][hpad]
-    off = align256(off + G * 2 * q.bpad * q.hpad * sizeof(uint16_t));
+    q.off_xhl = off;     // x split into bf16 high and low parts: [G][2][tok][hpad]
+    off = align256(off + G * 2 * q.tok * q.hpad * sizeof(uint16_t));
     q.off_cnt = off;     // per tile: |union G|, |union A|
     off = align256(off + G * T * 2 * sizeof(int32_t));
-    q.off_aseg = off;    // per tile: union-active rows
-    off = align256(off + G * T * kBxRows * sizeof(int32_t));
-    q.off_hseg = off;    // per tile row: Combined for each token
-    off = align256(off + G * T * kBxRows * q.bpad * sizeof(float));
+    q.off_arow = off;    // per tile: row (within the tile) of each of its 32 active slots, bytes
+    off = align256(off + G * T * kBxRows);
+    q.off_hfrag = off;   // per tile: Combined as bf16 high / low, [2][tok][32 slots]
+    off = align256(off + G * T * 2 * q.tok * kBxRows * sizeof(uint16_t));
     q.off_gmask = off;   // per tile and token: open-gate rows (bit mask)
-    off = align256(off + G * T * q.bpad * sizeof(uint32_t));
+    off = align256(off + G * T * q.tok * sizeof(uint32_t));
     q.off_amask = off;   // per tile and token: active rows (bit mask)
-    off = align256(off + G * T * q.bpad * sizeof(uint32_t));
-    q.off_partial = off; // down partials: [G][bpad][nchunks][hidden]
-    off = align256(off + G * q.bpad * (size_t)q.nchunks * hidden * sizeof(float));
+    off = align256(off + G * T * q.tok * sizeof(uint32_t));
+    q.off_partial = off; // down partials: [G][tok][nchunks][hidden]
+    off = align256(off + G * q.tok * (size_t)q.nchunks * hidden * sizeof(float));
     q.off_union = off;
     off = align256(off + 4 * sizeof(int32_t));
     q.total = off;

@@ -59,20 +59,21 @@ struct SlotPlan {
 // FFN has one group holding the batch, the MoE layer one group per expert
 // holding the tokens routed to it.
 constexpr int kBxMaxTokens = 64;  // tokens per group and pass
-constexpr int kBxRows = 32;       // neurons per gate+up wave tile
-constexpr int kBxSliceCols = 256; // output columns per down workgroup
-constexpr int kBxBlockRows = 32;  // down rows per MFMA K block
+constexpr int kBxRows = 32;       // neurons per gate+up workgroup tile (and per down K block)
+constexpr int kBxSliceCols = 128; // output columns per down wave
+constexpr int kBxChunkTiles = 64; // gate+up tiles per down chunk (one wave ballot)
+constexpr int kBxKQuant = 1024;   // the hidden dimension is padded to this (4 waves x 2 batches x 128)
 
 struct BatchPlan {
     int batch = 0, hidden = 0, inter = 0, groups = 1, top_k = 1;
-    int bpad = 0;        // tokens per group rounded up to 16 (MFMA N tile)
-    int nt = 0;          // 16-token tiles: bpad / 16
-    int hpad = 0;        // hidden rounded up to 64 (gate / up K blocks)
-    int ntiles = 0;      // 32-row wave tiles per group
-    int nslices = 0;     // 256-column slices of the down kernel
+    int tok = 0;         // token slots per group: 8 (high / low x parts share one MFMA tile), 16, 32 or 64
+    int bpad = 0;        // = tok
+    int hpad = 0;        // hidden rounded up to kBxKQuant (gate / up K range, zero x past hidden)
+    int ntiles = 0;      // 32-neuron tiles per group
+    int nslices = 0;     // 128-column slices of the down kernel
     int nchunks = 0;     // tile chunks per group in the down kernel
-    int tpc = 0;         // tiles per chunk
-    size_t off_gcount = 0, off_gtok = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_aseg = 0, off_hseg = 0;
+    int tpc = 0;         // tiles per chunk (<= kBxChunkTiles)
+    size_t off_gcount = 0, off_gtok = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_arow = 0, off_hfrag = 0;
     size_t off_gmask = 0, off_amask = 0, off_partial = 0, off_union = 0;
     size_t total = 0;
 };
