@@ -198,6 +198,9 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *   "down_chunks" tile groups per slot in the split path's down kernel
  *   "rif"        weight rows in flight per wave in the row dot products
  *                (1 or 2)
+ *   "bx_gate"    load shape of the batched gate+up kernel for up to 16
+ *                tokens per group: 0 default (4 k-steps of 32 per batch, 2
+ *                batches in flight), 1 = 2 x 2, 2 = 2 x 4
  * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
  */
 ts_status ts_tune_set(const char *key, int value);

@@ -72,8 +72,8 @@ struct Bx {
     static constexpr bool PACK = TOK == 8;          // high and low parts share one 16-column tile
     static constexpr int NT = PACK ? 1 : TOK / 16;  // 16-token accumulator tiles
     static constexpr int NX = PACK ? 1 : 2 * NT;    // operand fragments per 32-wide k-step (x or Combined)
-    static constexpr int KS = NX <= 2 ? 4 : 2;      // k-steps per batch of gate / up loads
-    static constexpr int D = 2;                     // gate / up batches in flight per wave
+    static constexpr int KS = NX <= 2 ? 4 : 2;      // k-steps per batch of gate / up loads (default)
+    static constexpr int D = 2;                     // gate / up batches in flight per wave (default)
     static constexpr int DD = 2;                    // down tiles in flight per wave
 };
 
@@ -87,7 +87,7 @@ struct BxArgs {
     int32_t *gcount;         // [G]
     int32_t *gtok;           // [G][bpad] token of each slot, -1 past the count
     int32_t *tslot;          // [B][K][2] (group, slot) of each routed token
-    uint16_t *xhl;           // [G][2][bpad][hpad]
+    uint16_t *xhl;           // x fragments [G][hpad / 32][NX][64 lanes][8] bf16 (MFMA operand order)
     int32_t *cnt;            // [G][ntiles][2] |union G|, |union A|
     uint8_t *arow;           // [G][ntiles][32] row within the tile of each active slot (slot 0's past |union A|)
     uint16_t *hfrag;         // [G][ntiles][2][bpad][32] Combined per active slot, bf16 high / low
@@ -139,53 +139,109 @@ __global__ __launch_bounds__(64) void bx_dispatch(BxArgs a) {
     for (int e = lane; e < a.G; e += 64) a.gcount[e] = s_base[e];
 }
 
-// x rows of each group's slots, split into bf16 high / low parts, zero past
-// the token count and past H (to hpad).  One block per (group, slot).
+// x of each group's token slots as MFMA operand fragments: for k-step ks (32
+// wide) and fragment f, lane (lm, lq) holds the 8 values at k = 32 ks + 8 lq
+// of column lm, column = (high or low part, token slot); fragments are 1 KB
+// contiguous, so a wave loads one with a single fully coalesced instruction.
+// Zero past the token count and past H (to hpad).  One thread per (group,
+// k-step, fragment, lane).  Without a routing table (the FFN) the slots are
+// the tokens themselves and block 0 also writes the group table.
+template <int TOK>
 __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
-    const int g = blockIdx.x / a.bpad;
-    const int s = blockIdx.x % a.bpad;
-    const int t = a.gtok[g * a.bpad + s];
-    uint16_t *hi = a.xhl + ((size_t)(g * 2) * a.bpad + s) * a.hpad;
-    uint16_t *lo = a.xhl + ((size_t)(g * 2 + 1) * a.bpad + s) * a.hpad;
-    for (int k = threadIdx.x; k < a.hpad; k += 256) {
-        const float v = (t >= 0 && k < a.H) ? a.x[(size_t)t * a.H + k] : 0.f;
-        uint32_t h, l;
-        split_hi_lo(v, h, l);
-        hi[k] = (uint16_t)h;
-        lo[k] = (uint16_t)l;
+    using S = Bx<TOK>;
+    constexpr int NX = S::NX;
+    if (!a.topk && blockIdx.x == 0) {
+        for (int t = threadIdx.x; t < a.B; t += 256) {
+            a.tslot[t * 2] = 0;
+            a.tslot[t * 2 + 1] = t;
+        }
+        if (threadIdx.x == 0) a.gcount[0] = a.B;
     }
+    const int nks = a.hpad / 32;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= a.G * nks * NX * 64) return;
+    const int lane = idx & 63, lm = lane & 15, lq = lane >> 4;
+    const int f = (idx >> 6) % NX;
+    const int ks = (idx >> 6) / NX % nks;
+    const int g = (idx >> 6) / NX / nks;
+    const int hl = S::PACK ? (lm >> 3) : (f & 1);
+    const int slot = S::PACK ? (lm & 7) : 16 * (f >> 1) + lm;
+    const int t = a.topk ? a.gtok[g * TOK + slot] : (slot < a.B ? slot : -1);
+    const int k0 = ks * 32 + 8 * lq;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (t >= 0 && k0 < a.H) {  // H is a multiple of 8, so all 8 are in range
+        const f32x4 *src = reinterpret_cast<const f32x4 *>(a.x + (size_t)t * a.H + k0);
+        const f32x4 p = src[0], q = src[1];
+        v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w;
+        v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        uint32_t h0, l0, h1, l1;
+        split_hi_lo(v[2 * e], h0, l0);
+        split_hi_lo(v[2 * e + 1], h1, l1);
+        o[e] = hl ? (l0 | (l1 << 16)) : (h0 | (h1 << 16));
+    }
+    reinterpret_cast<u32x4 *>(a.xhl)[idx] = u32x4{o[0], o[1], o[2], o[3]};
 }
 
 // ---------------------------------------------------------------------------
-// K loop of the gate / up contraction of one wave: MT 16-row m-tiles (row
-// pointer per lane: row lm of each m-tile) against the NX operand fragments
-// of x (pointer per lane: column lm of each fragment), over nbat batches of
-// KS k-steps starting at k-step ks0.  k-step s covers 64 contiguous bytes of
-// each row: lane (lm, lq) takes the 16 bytes at k = 32 s + 8 lq for both
-// operands, so each MFMA pairs matching K indices.  The loads of the next
-// D - 1 batches are in flight while a batch is contracted (registers used
-// as a ring, no copies).  Weight chunks past H re-read the row's last chunk;
-// x is zero there.
-template <int TOK, int MT>
-__device__ __forceinline__ void bx_kloop(const uint16_t *const (&wrow)[MT], int H,
-                                         const uint16_t *const (&xrow)[Bx<TOK>::NX], int ks0, int nbat, int lq,
+// K loop of the gate / up contraction of one wave: MT 16-row m-tiles against
+// the NX x fragments, over nbat batches of KS k-steps (32 wide) starting at
+// k-step ks0.  A batch spans CPR = 4 KS 16-byte chunks of each of the 16 MT
+// rows and is loaded RPI = 16 / KS rows per instruction (CPR lanes per row,
+// so every instruction reads whole 128-byte lines: 256 or 128 contiguous
+// bytes per row); wrow[j] is this lane's row for instruction j.  The chunks
+// go to the wave's own LDS region, chunk c of row r at position
+// swz(r, c), and come back as MFMA operands (lane (lm, lq) of k-step s:
+// row 16 mt + lm, chunk 4 s + lq); the swizzle spreads both the writes and
+// the 16 rows of a read over all banks.  x fragments are loaded directly
+// (1 KB contiguous each).  The loads of the next D - 1 batches are in
+// flight while a batch is contracted.  Chunks past H re-read the row's last
+// chunk; x is zero there.
+template <int KS>
+__device__ __forceinline__ int bx_swz(int r, int c) {
+    return KS == 4 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+}
+
+template <int TOK, int MT, int KS, int D>
+__device__ __forceinline__ void bx_kloop(const char *wbase, const uint32_t (&roff)[MT * KS], int H,
+                                         const u32x4 *__restrict__ xg, int ks0, int nbat, int lane, u32x4 *sw,
                                          f32x4 (&acc)[MT][Bx<TOK>::NT]) {
     using S = Bx<TOK>;
-    constexpr int KS = S::KS, D = S::D, NX = S::NX;
-    u32x4 w[D][MT][KS], xv[D][NX][KS];
+    constexpr int NX = S::NX, CPR = 4 * KS, RPI = 16 / KS, NI = MT * KS;
+    const int lm = lane & 15, lq = lane >> 4;
+    const int lc = lane % CPR, lr = lane / CPR;
+    u32x4 w[D][NI], xv[D][NX][KS];
+    // weights: uniform base + 32-bit per-lane byte offset (row * H * 2 + k * 2)
     auto issue = [&](int d, int b) {
-        const int kb = (ks0 + b * KS) * 32 + 8 * lq;
+        const int kb = (ks0 + b * KS) * 32;
+        const int k = kb + 8 * lc;
+        const uint32_t kw = 2u * (uint32_t)(k < H ? k : H - 8);
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            const int k = kb + 32 * s;
-            const int kw = k < H ? k : H - 8;
+        for (int j = 0; j < NI; ++j) w[d][j] = ld_stream(wbase + (roff[j] + kw));
+        const u32x4 *xb = xg + (size_t)(ks0 + b * KS) * NX * 64;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) w[d][mt][s] = ld_stream(wrow[mt] + kw);
+        for (int s = 0; s < KS; ++s)
 #pragma unroll
-            for (int f = 0; f < NX; ++f) xv[d][f][s] = ld_cached(xrow[f] + k);
-        }
+            for (int f = 0; f < NX; ++f) xv[d][f][s] = ld_cached(xb + (s * NX + f) * 64 + lane);
     };
     auto mma = [&](int d) {
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int r = RPI * j + lr;
+            sw[r * CPR + bx_swz<KS>(r, lc)] = w[d][j];
+        }
+        __builtin_amdgcn_wave_barrier();
+        u32x4 av[MT][KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const int r = 16 * mt + lm;
+                av[mt][s] = sw[r * CPR + bx_swz<KS>(r, 4 * s + lq)];
+            }
 #pragma unroll
         for (int s = 0; s < KS; ++s)
 #pragma unroll
@@ -193,13 +249,15 @@ __device__ __forceinline__ void bx_kloop(const uint16_t *const (&wrow)[MT], int 
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     f32x4 &c = acc[mt][S::PACK ? 0 : f >> 1];
-                    c = mfma_bf16(w[d][mt][s], xv[d][f][s], c);
+                    c = mfma_bf16(av[mt][s], xv[d][f][s], c);
                 }
+        __builtin_amdgcn_wave_barrier();
     };
-    // nbat is a positive multiple of D; the steady loop has no branch, so
-    // the waits before each batch's MFMAs leave the later batches in flight
-    // (the scheduling barriers keep each batch's loads together and in ring
-    // order, so a wait for one batch does not also wait for the next)
+    // nbat is a positive multiple of D (hpad is a multiple of 4 waves x 32 x
+    // KS x D).  The steady loop has no branch and the ring registers need no
+    // copies, so the waits before each batch's MFMAs leave the later batches
+    // in flight; the scheduling barriers keep each batch's loads together
+    // and in ring order.
 #pragma unroll
     for (int d = 0; d < D; ++d) {
         issue(d, d);
@@ -302,13 +360,15 @@ __device__ __forceinline__ int nth_set_bit(uint32_t m, int n) {
     return pos;
 }
 
-template <int TOK>
-__global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
+template <int TOK, int KS, int D>
+__global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
     using S = Bx<TOK>;
     constexpr int NT = S::NT, NX = S::NX;
+    constexpr int CPR = 4 * KS, RPI = 16 / KS;
     __shared__ f32x4 s_red[4][2][NT][64];
     __shared__ float s_g[kBxRows][TOK];
     __shared__ __attribute__((aligned(16))) uint16_t s_h[2 * TOK][kBxRows];
+    __shared__ u32x4 s_stage[4][kBxRows * CPR];  // per-wave weight staging
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
@@ -334,14 +394,12 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
     const int r0 = tile * kBxRows;
     const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)g * a.expert_stride;
     const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)g * a.expert_stride;
-    const uint16_t *xrow[NX];
-#pragma unroll
-    for (int f = 0; f < NX; ++f) {
-        const size_t r = S::PACK ? (size_t)g * 16 + lm : ((size_t)(g * 2 + (f & 1)) * TOK + 16 * (f >> 1) + lm);
-        xrow[f] = a.xhl + r * a.hpad;
-    }
-    const int kpw = a.hpad / 128;  // k-steps per wave (hpad / 32 over 4 waves)
-    const int ks0 = wave * kpw, nbat = kpw / S::KS;
+    const int nks = a.hpad / 32;
+    const u32x4 *xg = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * nks * NX * 64;
+    const int kpw = nks / 4;  // k-steps per wave
+    const int ks0 = wave * kpw, nbat = kpw / KS;
+    u32x4 *sw = s_stage[wave];
+    const int lr = lane / CPR;  // row of this lane within an instruction's RPI rows
     // token of this lane's accumulator column, and whether the lane reports it
     const bool tok_lane = !S::PACK || lm < 8;
 
@@ -352,10 +410,10 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     {
-        const uint16_t *rows[2];
+        uint32_t roff[2 * KS];
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) rows[mt] = wg + (size_t)min(r0 + 16 * mt + lm, a.I - 1) * a.H;
-        bx_kloop<TOK, 2>(rows, a.H, xrow, ks0, nbat, lq, acc);
+        for (int j = 0; j < 2 * KS; ++j) roff[j] = 2u * (uint32_t)min(r0 + RPI * j + lr, a.I - 1) * (uint32_t)a.H;
+        bx_kloop<TOK, 2, KS, D>(reinterpret_cast<const char *>(wg), roff, a.H, xg, ks0, nbat, lane, sw, acc);
     }
     bx_combine<NT>(acc, s_red, wave, lane);
     bx_pair_sum<TOK>(acc);
@@ -392,19 +450,24 @@ __global__ __launch_bounds__(256) void bx_gate_up(BxArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) uacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (nu > 16) {
-        const uint16_t *rows[2];
+        uint32_t roff[2 * KS];
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
-            const int j = 16 * mt + lm;
-            rows[mt] = wu + (size_t)(r0 + nth_set_bit(umask, j < nu ? j : 0)) * a.H;
+        for (int j = 0; j < 2 * KS; ++j) {
+            const int u = RPI * j + lr;
+            roff[j] = 2u * (uint32_t)(r0 + nth_set_bit(umask, u < nu ? u : 0)) * (uint32_t)a.H;
         }
-        bx_kloop<TOK, 2>(rows, a.H, xrow, ks0, nbat, lq, uacc);
+        bx_kloop<TOK, 2, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, uacc);
     } else if (nu > 0) {
-        const uint16_t *rows[1] = {wu + (size_t)(r0 + nth_set_bit(umask, lm < nu ? lm : 0)) * a.H};
+        uint32_t roff[KS];
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            const int u = RPI * j + lr;
+            roff[j] = 2u * (uint32_t)(r0 + nth_set_bit(umask, u < nu ? u : 0)) * (uint32_t)a.H;
+        }
         f32x4 u1[1][NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) u1[0][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        bx_kloop<TOK, 1>(rows, a.H, xrow, ks0, nbat, lq, u1);
+        bx_kloop<TOK, 1, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, u1);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) uacc[0][nt] = u1[0][nt];
     }
@@ -750,9 +813,26 @@ T *ws_at(void *ws, size_t off) {
     return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
 }
 
+// gate+up load shape: k-steps per batch x batches in flight ("bx_gate" knob,
+// 0 = the default for the token count)
+template <int TOK>
+void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
+    const dim3 grid((unsigned)(p.groups * p.ntiles));
+    if constexpr (TOK <= 16) {
+        switch (tuned("bx_gate")) {
+        case 1: launch("batch_gate_up", bx_gate_up<TOK, 2, 2>, grid, dim3(256), st, a); return;
+        case 2: launch("batch_gate_up", bx_gate_up<TOK, 2, 4>, grid, dim3(256), st, a); return;
+        default: break;
+        }
+    }
+    launch("batch_gate_up", bx_gate_up<TOK, Bx<TOK>::KS, Bx<TOK>::D>, grid, dim3(256), st, a);
+}
+
 template <int TOK>
 void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
-    launch("batch_gate_up", bx_gate_up<TOK>, dim3((unsigned)(p.groups * p.ntiles)), dim3(256), st, a);
+    const int nthreads = p.groups * (p.hpad / 32) * Bx<TOK>::NX * 64;
+    launch("batch_prep", bx_prep<TOK>, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), st, a);
+    launch_gate_up<TOK>(p, a, st);
     launch("batch_down", bx_down<TOK>, dim3((unsigned)(p.groups * p.nchunks * p.nslices)), dim3(256), st, a);
 }
 
@@ -798,8 +878,7 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     const bool want_lists = stats && (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx);
     a.want_masks = want_lists ? 1 : 0;
 
-    launch("batch_dispatch", bx_dispatch, dim3(1), dim3(64), st, a);
-    launch("batch_prep", bx_prep, dim3((unsigned)(p.groups * p.bpad)), dim3(256), st, a);
+    if (topk) launch("batch_dispatch", bx_dispatch, dim3(1), dim3(64), st, a);
     switch (p.tok) {
     case 8: launch_tok<8>(p, a, st); break;
     case 16: launch_tok<16>(p, a, st); break;

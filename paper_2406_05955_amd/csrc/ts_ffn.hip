@@ -1201,10 +1201,13 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
     if (s != TS_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
     // Several tokens with bf16 weights: the batched matrix-core path, in
-    // passes of up to 64 tokens (the union count needs a single pass).
+    // passes of up to 64 tokens (the union count needs a single pass);
+    // shapes it does not take run the single-token kernels per token.
     const bool one_pass = batch <= ts::kBxMaxTokens;
+    ts::BatchPlan probe;
     if (batch > 1 && wdtype == TS_BF16 && ts::tuned("batch_path") == 0 &&
-        (one_pass || !(stats && stats->n_union))) {
+        (one_pass || !(stats && stats->n_union)) &&
+        ts::plan_batch(std::min(batch, ts::kBxMaxTokens), hidden, inter, 1, 1, wdtype, &probe)) {
         for (int t0 = 0; t0 < batch; t0 += ts::kBxMaxTokens) {
             const int nb = std::min(ts::kBxMaxTokens, batch - t0);
             ts::BatchPlan bp;
@@ -1225,7 +1228,9 @@ ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, con
                                      ws_bytes, &p);
     if (s != TS_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (batch > 1 && wdtype == TS_BF16 && ts::tuned("batch_path") == 0) {
+    ts::BatchPlan probe;
+    if (batch > 1 && wdtype == TS_BF16 && ts::tuned("batch_path") == 0 &&
+        ts::plan_batch(std::min(batch, ts::kBxMaxTokens), hidden, inter, 1, 1, wdtype, &probe)) {
         for (int t0 = 0; t0 < batch; t0 += ts::kBxMaxTokens) {
             const int nb = std::min(ts::kBxMaxTokens, batch - t0);
             ts::BatchPlan bp;

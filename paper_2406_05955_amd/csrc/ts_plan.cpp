@@ -14,6 +14,7 @@ std::atomic<int> g_down_chunks{0};
 std::atomic<int> g_path{0};
 std::atomic<int> g_rif{0};
 std::atomic<int> g_batch{0};
+std::atomic<int> g_bx_gate{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
@@ -30,6 +31,7 @@ int tuned(const char *key) {
     if (std::strcmp(key, "ffn_path") == 0) return g_path.load();
     if (std::strcmp(key, "rif") == 0) return g_rif.load();
     if (std::strcmp(key, "batch_path") == 0) return g_batch.load();
+    if (std::strcmp(key, "bx_gate") == 0) return g_bx_gate.load();
     return 0;
 }
 
@@ -155,6 +157,8 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
 bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p) {
     if (check_dims(batch, hidden, inter, dt) != TS_OK || dt != TS_BF16 || groups < 1 || top_k < 1) return false;
     if (batch > kBxMaxTokens) return false;
+    // the gate / up kernel addresses rows with 32-bit byte offsets into one matrix
+    if ((unsigned long long)inter * (unsigned long long)hidden * 2ull >= (1ull << 32)) return false;
     BatchPlan q;
     q.batch = batch;
     q.hidden = hidden;
@@ -286,6 +290,11 @@ ts_status ts_tune_set(const char *key, int value) {
     if (std::strcmp(key, "batch_path") == 0) {
         if (value < 0 || value > 1) return TS_ERR_SHAPE;
         ts::g_batch.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "bx_gate") == 0) {
+        if (value < 0 || value > 2) return TS_ERR_SHAPE;
+        ts::g_bx_gate.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;
