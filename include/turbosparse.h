@@ -201,6 +201,8 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *   "bx_gate"    load shape of the batched gate+up kernel for up to 16
  *                tokens per group: 0 default (4 k-steps of 32 per batch, 2
  *                batches in flight), 1 = 2 x 2, 2 = 2 x 4
+ *   "bx_down"    batched down kernel for up to 16 tokens per group: 0 default
+ *                (2 blocks of 32 rows in flight per wave), 1 = 3 blocks
  * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
  */
 ts_status ts_tune_set(const char *key, int value);

@@ -74,7 +74,7 @@ struct Bx {
     static constexpr int NX = PACK ? 1 : 2 * NT;    // operand fragments per 32-wide k-step (x or Combined)
     static constexpr int KS = NX <= 2 ? 4 : 2;      // k-steps per batch of gate / up loads (default)
     static constexpr int D = 2;                     // gate / up batches in flight per wave (default)
-    static constexpr int DD = 2;                    // down tiles in flight per wave
+    static constexpr int DD = 2;                    // down blocks in flight per wave (default)
 };
 
 struct BxArgs {
@@ -90,7 +90,7 @@ struct BxArgs {
     uint16_t *xhl;           // x fragments [G][hpad / 32][NX][64 lanes][8] bf16 (MFMA operand order)
     int32_t *cnt;            // [G][ntiles][2] |union G|, |union A|
     uint8_t *arow;           // [G][ntiles][32] row within the tile of each active slot (slot 0's past |union A|)
-    uint16_t *hfrag;         // [G][ntiles][2][bpad][32] Combined per active slot, bf16 high / low
+    uint16_t *hfrag;         // [G][ntiles][32 slots][2][bpad] Combined per active slot, bf16 high / low
     uint32_t *gmask;         // [G][ntiles][bpad] open-gate rows of the tile per token
     uint32_t *amask;         // [G][ntiles][bpad] active rows of the tile per token
     float *partial;          // [G][bpad][nchunks][H]
@@ -367,7 +367,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
     constexpr int CPR = 4 * KS, RPI = 16 / KS;
     __shared__ f32x4 s_red[4][2][NT][64];
     __shared__ float s_g[kBxRows][TOK];
-    __shared__ __attribute__((aligned(16))) uint16_t s_h[2 * TOK][kBxRows];
+    __shared__ __attribute__((aligned(16))) uint16_t s_h[kBxRows][2 * TOK];
     __shared__ u32x4 s_stage[4][kBxRows * CPR];  // per-wave weight staging
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -517,8 +517,8 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
                         const int t = S::PACK ? lm : 16 * nt + lm;
                         uint32_t hi, lo;
                         split_hi_lo(hv[mt][nt][i], hi, lo);
-                        s_h[t][slot] = (uint16_t)hi;
-                        s_h[TOK + t][slot] = (uint16_t)lo;
+                        s_h[slot][t] = (uint16_t)hi;
+                        s_h[slot][TOK + t] = (uint16_t)lo;
                     }
                 }
             }
@@ -539,28 +539,41 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Down: workgroup (group, chunk of tiles, 128-column slice), 4 waves; wave w
-// takes every 4th non-empty tile of the chunk.  A tile is one K block of 32
-// slots: its active W_down_t rows (slots past |union A| repeat slot 0's row,
-// with zero Combined) x the slice's 128 columns, 8 KB loaded as 8 coalesced
-// 16-byte loads per lane (lane (lq, lm): slot 4q + lq, columns 8 lm..8 lm+7)
-// and written to the wave's own LDS region row-major, the 16-byte chunk c
-// of slot s stored at position c ^ (2 ((s >> 3) & 3)).  The MFMA operand of
-// n-tile nc (columns 16 nc + lm) takes slots 8 lq .. 8 lq + 7 of one column:
-// eight 2-byte LDS reads whose 16 lanes of each lq hit 8 banks of their own
-// (the swizzle moves the four lq groups apart), so neither the writes nor
-// the reads conflict.  The other operand is the tile's Combined fragment
-// (token rows, slots contiguous) as written by bx_gate_up.  Loads of the
-// next DD - 1 tiles are in flight while a tile is contracted.
-template <int TOK>
+// Down: workgroup (group, chunk of tiles, 128-column slice), 4 waves.  The
+// chunk's active rows, tile after tile in ascending order, are listed once
+// in LDS (row, and where its Combined values are) and cut into K blocks of
+// 32; wave w takes blocks w, w + 4, ...  A block's W_down_t rows x the
+// slice's 128 columns (8 KB) are loaded as 8 coalesced 16-byte loads per
+// lane (lane (lq, lm): slot 8 lq + q, columns 8 lm .. 8 lm + 7) and written
+// to the wave's own LDS region row-major, the 16-byte chunk c of slot s at
+// position c ^ (2 ((s >> 3) & 3)).  The MFMA operand of n-tile nc (columns
+// 16 nc + lm) takes slots 8 lq .. 8 lq + 7 of one column: eight 2-byte LDS
+// reads whose 16 lanes of each lq hit 8 banks of their own (the swizzle
+// moves the four lq groups apart), so neither the writes nor the reads
+// conflict.  The block's Combined values (slot-major records written by
+// bx_gate_up) are transposed through a small LDS tile into the other
+// operand (token rows, 8 consecutive slots per lane).  Slots past the last
+// row repeat a listed row with zero Combined.  Loads of the next DD - 1
+// blocks are in flight while a block is contracted; the four waves' sums
+// are added in a fixed order at the end.
+template <int TOK, int DD>
 __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     using S = Bx<TOK>;
-    constexpr int NT = S::NT, NX = S::NX, DD = S::DD;
+    constexpr int NT = S::NT, NX = S::NX;
     constexpr int REG = 512 * NT;  // 16-byte units per wave: 8 KB staging, or its 8 x NT accumulators
     constexpr int BG = 2;          // n-tiles whose operands are read from LDS together
+    constexpr int AP = 40;         // bf16 per row of the Combined tile (80 bytes: 16-row reads do not conflict)
+    constexpr int HC = TOK / 8;    // 16-byte Combined chunks per lane (token half of one slot)
+    constexpr int MAXR = kBxChunkTiles * kBxRows;
     __shared__ u32x4 s_lds[4 * REG];
+    __shared__ __attribute__((aligned(16))) uint32_t s_row[MAXR];  // listed rows (index within the group)
+    __shared__ int32_t s_hix[MAXR];                                // their Combined record, -1 = padding
+    __shared__ int s_pre[kBxChunkTiles + 1];
+    // the Combined tile: past the staging 8 KB of the wave's region when it has room (NT >= 2)
+    constexpr bool AIN = NT >= 2;
+    __shared__ __attribute__((aligned(16))) uint16_t s_a_own[AIN ? 1 : 4][2 * TOK][AP];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
     const int slice = blockIdx.x % a.nslices;
     const int chunk = (blockIdx.x / a.nslices) % a.nchunks;
@@ -572,46 +585,44 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     const int ntc = min(a.tpc, a.ntiles - t0);
     const size_t tbase = (size_t)g * a.ntiles + t0;
 
-    // lane t: |union A| and slot rows of the chunk's tile t
-    int na_l = 0;
-    u32x4 rt0 = {0u, 0u, 0u, 0u}, rt1 = {0u, 0u, 0u, 0u};
-    if (lane < ntc) {
-        na_l = a.cnt[(tbase + lane) * 2 + 1];
-        rt0 = *reinterpret_cast<const u32x4 *>(a.arow + (tbase + lane) * kBxRows);
-        rt1 = *reinterpret_cast<const u32x4 *>(a.arow + (tbase + lane) * kBxRows + 16);
+    // ---- the chunk's row list ---------------------------------------------
+    if (wave == 0) {
+        const int na = lane < ntc ? a.cnt[(tbase + lane) * 2 + 1] : 0;
+        int inc = na;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(inc, o, 64);
+            if (lane >= o) inc += v;
+        }
+        if (lane < ntc) s_pre[lane] = inc - na;
+        if (lane == 63) s_pre[ntc] = inc;
     }
-    const uint64_t ne = __ballot(na_l > 0);
-    const bool mine = ((ne >> lane) & 1ull) && (lane_prefix(ne, lane) & 3) == wave;
-    uint64_t mq = __ballot(mine);  // this wave's tiles, taken lowest first
-    const int nblk = __popcll(mq);
+    __syncthreads();
+    const int total = s_pre[ntc];
+    for (int e = tid; e < ntc * kBxRows; e += 256) {
+        const int t = e / kBxRows, sl = e % kBxRows;
+        const int base = s_pre[t];
+        if (sl < s_pre[t + 1] - base) {
+            s_row[base + sl] = (uint32_t)((t0 + t) * kBxRows + a.arow[(tbase + t) * kBxRows + sl]);
+            s_hix[base + sl] = (int32_t)((tbase + t) * kBxRows + sl);
+        }
+    }
+    const int nblk = (total + kBxRows - 1) / kBxRows;
+    __syncthreads();
+    for (int e = total + tid; e < nblk * kBxRows; e += 256) {
+        s_row[e] = s_row[0];
+        s_hix[e] = -1;
+    }
+    __syncthreads();
 
-    const uint16_t *wd = reinterpret_cast<const uint16_t *>(a.wd) + (size_t)g * a.expert_stride;
+    const char *wd = reinterpret_cast<const char *>(reinterpret_cast<const uint16_t *>(a.wd) + (size_t)g * a.expert_stride);
     const int col0 = slice * kBxSliceCols;
-    const int cw = min(col0 + 8 * lm, H - 8);
+    const uint32_t cw = 2u * (uint32_t)min(col0 + 8 * lm, H - 8);
+    const uint32_t H2 = 2u * (uint32_t)H;
     u32x4 *sw = s_lds + wave * REG;
     const uint16_t *sw16 = reinterpret_cast<const uint16_t *>(sw);
-
-    u32x4 wv[DD][8], hq[DD][NX];
-    // tiles are issued in order; with none left (prologue of a wave with
-    // fewer than DD tiles) tile 0 of the chunk is loaded and never used
-    auto issue = [&](int d) {
-        const int t = mq ? __builtin_ctzll(mq) : 0;
-        mq &= mq - 1ull;
-        const uint32_t tr[8] = {rt0.x, rt0.y, rt0.z, rt0.w, rt1.x, rt1.y, rt1.z, rt1.w};
-        const size_t rowbase = (size_t)(t0 + t) * kBxRows;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const uint32_t wq = (uint32_t)__builtin_amdgcn_readlane((int)tr[q], t);
-            const int rr = (int)((wq >> (8 * lq)) & 0xFFu);
-            wv[d][q] = ld_stream(wd + (rowbase + rr) * H + cw);
-        }
-        const uint16_t *hb = a.hfrag + (tbase + t) * (2 * TOK * kBxRows);
-#pragma unroll
-        for (int f = 0; f < NX; ++f) {
-            const int fr = S::PACK ? lm : (f & 1) * TOK + 16 * (f >> 1) + lm;
-            hq[d][f] = ld_cached(hb + fr * kBxRows + 8 * lq);
-        }
-    };
+    uint16_t(*s_a)[AP] = AIN ? reinterpret_cast<uint16_t(*)[AP]>(sw + 512) : s_a_own[AIN ? 0 : wave];
+    const int hj = lane & 31, hh = lane >> 5;  // Combined staging: slot, token half (high / low part)
 
     f32x4 acc[8][NT];
 #pragma unroll
@@ -619,59 +630,91 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[nc][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto mma = [&](int d) {
+    const int nbw = nblk > wave ? (nblk - wave + 3) / 4 : 0;  // this wave's blocks
+    if (nbw > 0) {
+        u32x4 wv[DD][8], hq[DD][HC];
+        bool hok[DD];
+        int kk = 0;  // blocks issued so far; past the last, block `wave` is re-read and never used
+        auto issue = [&](int d) {
+            const int bb = kk < nbw ? wave + 4 * kk : wave;
+            ++kk;
+            const u32x4 ra = *reinterpret_cast<const u32x4 *>(&s_row[bb * kBxRows + 8 * lq]);
+            const u32x4 rb = *reinterpret_cast<const u32x4 *>(&s_row[bb * kBxRows + 8 * lq + 4]);
+            const uint32_t rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int slot = 4 * q + lq;
-            sw[slot * 16 + (lm ^ (2 * ((slot >> 3) & 3)))] = wv[d][q];
-        }
-        __builtin_amdgcn_wave_barrier();
+            for (int q = 0; q < 8; ++q) wv[d][q] = ld_stream(wd + (rr[q] * H2 + cw));
+            const int hx = s_hix[bb * kBxRows + hj];
+            hok[d] = hx >= 0;
+            const uint16_t *hs = a.hfrag + (size_t)(hx >= 0 ? hx : 0) * (2 * TOK) + hh * TOK;
 #pragma unroll
-        for (int n2 = 0; n2 < 8; n2 += BG) {
-            u16x8 bfr[BG];
+            for (int c = 0; c < HC; ++c) hq[d][c] = ld_cached(hs + 8 * c);
+        };
+        auto mma = [&](int d) {
 #pragma unroll
-            for (int u = 0; u < BG; ++u) {
-                const int pos = (2 * (n2 + u) + (lm >> 3)) ^ (2 * lq);
-                const uint16_t *src = sw16 + (8 * lq) * kBxSliceCols + 8 * pos + (lm & 7);
+            for (int q = 0; q < 8; ++q) sw[(8 * lq + q) * 16 + (lm ^ (2 * lq))] = wv[d][q];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) bfr[u][j] = src[j * kBxSliceCols];
-            }
+            for (int c = 0; c < HC; ++c) {
+                const uint32_t w4[4] = {hq[d][c].x, hq[d][c].y, hq[d][c].z, hq[d][c].w};
 #pragma unroll
-            for (int u = 0; u < BG; ++u) {
-                const u32x4 b = __builtin_bit_cast(u32x4, bfr[u]);
-#pragma unroll
-                for (int f = 0; f < NX; ++f) {
-                    f32x4 &c = acc[n2 + u][S::PACK ? 0 : f >> 1];
-                    c = mfma_bf16(hq[d][f], b, c);
+                for (int e = 0; e < 8; ++e) {
+                    const uint16_t v = (uint16_t)(e & 1 ? w4[e >> 1] >> 16 : w4[e >> 1] & 0xFFFFu);
+                    s_a[hh * TOK + 8 * c + e][hj] = hok[d] ? v : (uint16_t)0;
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        __builtin_amdgcn_wave_barrier();
-    };
-
-    // steady loop without branches (every issue is a real tile), then the
-    // last (fewer than 2 DD) tiles
+            __builtin_amdgcn_wave_barrier();
+            u32x4 af[NX];
 #pragma unroll
-    for (int d = 0; d < DD; ++d) issue(d);
-    int b = 0;
-    for (; b + 2 * DD <= nblk; b += DD) {
+            for (int f = 0; f < NX; ++f) {
+                const int ar = S::PACK ? lm : (f & 1) * TOK + 16 * (f >> 1) + lm;
+                af[f] = *reinterpret_cast<const u32x4 *>(&s_a[ar][8 * lq]);
+            }
+#pragma unroll
+            for (int n2 = 0; n2 < 8; n2 += BG) {
+                u16x8 bfr[BG];
+#pragma unroll
+                for (int u = 0; u < BG; ++u) {
+                    const int pos = (2 * (n2 + u) + (lm >> 3)) ^ (2 * lq);
+                    const uint16_t *src = sw16 + (8 * lq) * kBxSliceCols + 8 * pos + (lm & 7);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) bfr[u][j] = src[j * kBxSliceCols];
+                }
+#pragma unroll
+                for (int u = 0; u < BG; ++u) {
+                    const u32x4 b = __builtin_bit_cast(u32x4, bfr[u]);
+#pragma unroll
+                    for (int f = 0; f < NX; ++f) {
+                        f32x4 &c = acc[n2 + u][S::PACK ? 0 : f >> 1];
+                        c = mfma_bf16(af[f], b, c);
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_wave_barrier();
+        };
+
+        // steady loop without branches (every issue is a real block), then
+        // the last (fewer than 2 DD) blocks
+#pragma unroll
+        for (int d = 0; d < DD; ++d) issue(d);
+        int b = 0;
+        for (; b + 2 * DD <= nbw; b += DD) {
+#pragma unroll
+            for (int d = 0; d < DD; ++d) {
+                mma(d);
+                issue(d);
+            }
+        }
 #pragma unroll
         for (int d = 0; d < DD; ++d) {
-            mma(d);
-            issue(d);
+            if (b + d < nbw) {
+                mma(d);
+                if (b + d + DD < nbw) issue(d);
+            }
         }
-    }
 #pragma unroll
-    for (int d = 0; d < DD; ++d) {
-        if (b + d < nblk) {
-            mma(d);
-            if (b + d + DD < nblk) issue(d);
-        }
+        for (int d = 0; d < DD; ++d)
+            if (b + DD + d < nbw) mma(d);
     }
-#pragma unroll
-    for (int d = 0; d < DD; ++d)
-        if (b + DD + d < nblk) mma(d);
 
     // the four waves' sums, added in a fixed order; wave w finishes n-tiles 2w, 2w + 1
     f32x4 *sa = reinterpret_cast<f32x4 *>(sw);
@@ -833,7 +876,14 @@ void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
     const int nthreads = p.groups * (p.hpad / 32) * Bx<TOK>::NX * 64;
     launch("batch_prep", bx_prep<TOK>, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), st, a);
     launch_gate_up<TOK>(p, a, st);
-    launch("batch_down", bx_down<TOK>, dim3((unsigned)(p.groups * p.nchunks * p.nslices)), dim3(256), st, a);
+    const dim3 grid((unsigned)(p.groups * p.nchunks * p.nslices));
+    if constexpr (TOK <= 16) {
+        if (tuned("bx_down") == 1) {
+            launch("batch_down", bx_down<TOK, 3>, grid, dim3(256), st, a);
+            return;
+        }
+    }
+    launch("batch_down", bx_down<TOK, Bx<TOK>::DD>, grid, dim3(256), st, a);
 }
 
 }  // namespace

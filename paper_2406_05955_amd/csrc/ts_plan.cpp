@@ -15,6 +15,7 @@ std::atomic<int> g_path{0};
 std::atomic<int> g_rif{0};
 std::atomic<int> g_batch{0};
 std::atomic<int> g_bx_gate{0};
+std::atomic<int> g_bx_down{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
@@ -32,6 +33,7 @@ int tuned(const char *key) {
     if (std::strcmp(key, "rif") == 0) return g_rif.load();
     if (std::strcmp(key, "batch_path") == 0) return g_batch.load();
     if (std::strcmp(key, "bx_gate") == 0) return g_bx_gate.load();
+    if (std::strcmp(key, "bx_down") == 0) return g_bx_down.load();
     return 0;
 }
 
@@ -295,6 +297,11 @@ ts_status ts_tune_set(const char *key, int value) {
     if (std::strcmp(key, "bx_gate") == 0) {
         if (value < 0 || value > 2) return TS_ERR_SHAPE;
         ts::g_bx_gate.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "bx_down") == 0) {
+        if (value < 0 || value > 1) return TS_ERR_SHAPE;
+        ts::g_bx_down.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;
