@@ -96,6 +96,21 @@ __device__ __forceinline__ u32x4 ld_stream_clamped(const void *row, int c, int n
     return ld_stream(static_cast<const char *>(row) + (size_t)cc * 16);
 }
 
+// Raw buffer resource over `bytes` bytes at `base` (gfx9 layout, 32-bit
+// dword format).  Loads through it at offsets past `bytes` return zeros and
+// touch no memory, so a masked load is an ordinary load at an out-of-range
+// offset: no branch, no traffic.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+constexpr uint32_t kOutOfRange = 0x80000000u;  // offset past every resource used here
+
+// Streaming (non-temporal) 16-byte load at byte offset `off` of resource `r`.
+__device__ __forceinline__ u32x4 ld_buf_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+}
+
 __device__ __forceinline__ f32x4 ld_f32x4_masked(const float *p, int i4, int n4) {
     const int ii = i4 < n4 ? i4 : n4 - 1;
     f32x4 v = *reinterpret_cast<const f32x4 *>(p + (size_t)ii * 4);

@@ -220,15 +220,19 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
 #pragma unroll
         for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
 
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(wd, (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT));
     for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
         u32x4 v[kDownUnroll][NCD];
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
             const int aa = a0 + u;
-            const WT *row = wd + (size_t)s_al[aa < na ? aa : a0] * H;
+            const uint32_t base =
+                aa < na ? (uint32_t)s_al[aa] * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
-            for (int kd = 0; kd < NCD; ++kd)
-                v[u][kd] = ld_stream_masked(row, tid + kThreads * kd, nch, 16, aa < na);
+            for (int kd = 0; kd < NCD; ++kd) {
+                const int c = tid + kThreads * kd;
+                v[u][kd] = ld_buf_stream(rd, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+            }
         }
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
@@ -280,19 +284,23 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
 template <typename WT, int NC>
 struct PipeWave {
     static constexpr int CE = WTraits<WT>::CE;
-    const WT *wg, *wu;
-    const void *dummy;  // x: an L2-resident row-sized buffer for unused load slots
+    __amdgpu_buffer_rsrc_t rg, ru;  // the tile's W_gate / W_up rows
     int H, nch, lane;
     float (&xr)[NC][CE];
     float *s_g, *s_h;
     int *s_on;
 
-    // Loads are unconditional (an unused slot reads `dummy`), so no branch
+    // Loads are unconditional: an unused slot (row < 0) and chunks past the
+    // row end read out of range (zeros, no memory traffic), so no branch
     // separates a load from its consumer and all of a wave's loads stay in
-    // flight across steps.  Chunks past the row end meet zero x values.
-    __device__ void issue(const void *row, u32x4 (&v)[NC]) {
+    // flight across steps.
+    __device__ void issue(__amdgpu_buffer_rsrc_t r, int row, u32x4 (&v)[NC]) {
+        const uint32_t base = row >= 0 ? (uint32_t)row * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
-        for (int c0 = 0; c0 < NC; ++c0) v[c0] = ld_stream_clamped(row, lane + 64 * c0, nch);
+        for (int c0 = 0; c0 < NC; ++c0) {
+            const int c = lane + 64 * c0;
+            v[c0] = ld_buf_stream(r, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+        }
     }
     __device__ float dot(const u32x4 (&v)[NC]) {
         float d = 0.f;
@@ -305,16 +313,17 @@ struct PipeWave {
         }
         return wave_sum(d);
     }
-    // One row: gate dot from gcur; issue the row's up loads into ucur (its
-    // W_up row if the gate is open); refill gcur with the row two ahead;
-    // finish the previous row's up dot from uprev (prev_row < 0: none).
-    // Steps past the wave's last row run on dummy data and change nothing.
+    // One row (tile-local index): gate dot from gcur; issue the row's up
+    // loads into ucur (its W_up row if the gate is open); refill gcur with
+    // the row two ahead; finish the previous row's up dot from uprev
+    // (prev_row < 0: none).  Steps past the wave's last row run on zeros and
+    // change nothing.
     __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC],
                          u32x4 (&uprev)[NC], int &prev_row) {
         const float g = dot(gcur);
         const bool open = valid && g > 0.f;
-        issue(open ? static_cast<const void *>(wu + (size_t)row * H) : dummy, ucur);
-        issue(next2 >= 0 ? static_cast<const void *>(wg + (size_t)next2 * H) : dummy, gcur);
+        issue(ru, open ? row : -1, ucur);
+        issue(rg, next2, gcur);
         if (lane == 0 && valid) {
             s_g[row] = g;
             s_on[row] = 0;
@@ -363,14 +372,16 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
 
     float xr[NC][CE];
     const float *xt = a.x + (size_t)tok * H;
-    PipeWave<WT, NC> pw{wg, wu, xt, H, nch, lane, xr, s_g, s_h, s_on};
+    // buffer resources over the tile's rows (at most 128 rows of 32 KB)
+    const uint32_t tbytes = (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT);
+    PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H, nch, lane, xr, s_g, s_h, s_on};
 
     // this wave's rows: wave, wave + 8, ...; first two gate rows in flight
     const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
     u32x4 g0[NC], g1[NC], u0[NC], u1[NC];
     load_x<WT, NC>(xt, lane, nch, xr);
-    pw.issue(nrow > 0 ? static_cast<const void *>(wg + (size_t)wave * H) : xt, g0);
-    pw.issue(nrow > 1 ? static_cast<const void *>(wg + (size_t)(wave + kWaves) * H) : xt, g1);
+    pw.issue(pw.rg, nrow > 0 ? wave : -1, g0);
+    pw.issue(pw.rg, nrow > 1 ? wave + kWaves : -1, g1);
 
     // MR (even) >= rows per wave; the loop is unrolled so every load is
     // issued in straight-line code.
@@ -424,15 +435,19 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     for (int kd = 0; kd < NCD; ++kd)
 #pragma unroll
         for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
+    const __amdgpu_buffer_rsrc_t rd = make_rsrc(wd, tbytes);
     for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
         u32x4 v[kDownUnroll][NCD];
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
             const int aa = a0 + u;
-            const WT *row = wd + (size_t)s_al[aa < na ? aa : a0] * H;
+            const uint32_t base =
+                aa < na ? (uint32_t)s_al[aa] * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
-            for (int kd = 0; kd < NCD; ++kd)
-                v[u][kd] = ld_stream_masked(row, tid + kThreads * kd, nch, 16, aa < na);
+            for (int kd = 0; kd < NCD; ++kd) {
+                const int c = tid + kThreads * kd;
+                v[u][kd] = ld_buf_stream(rd, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+            }
         }
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
@@ -923,8 +938,6 @@ void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs 
     }
 }
 
-// The pipelined kernel keeps x, two gate rows and two up rows in registers;
-// with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
 // The pipelined kernel keeps x, two gate rows and two up rows in registers;
 // with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
 // MR, the unrolled rows per wave, is the smallest of 2, 4, 8, 16 covering the tile.
