@@ -106,7 +106,40 @@ struct SlotArgs {
     int32_t *aseg;           // [slots][ntiles][tile] tile's A, ascending (if want_seg)
     float *partial;          // [slots][ntiles][H]
     int want_seg;
+    // In-kernel routing (pipelined kernel, route == null): router weights
+    // [E][H]; the tile-0 workgroup of each slot records its expert and
+    // renormalised weight in ridx / rw ([tokens][K]).
+    const void *wr;
+    int E, K;
+    int32_t *ridx;
+    float *rw;
 };
+
+// Softmax over the E logits, the top K (strictly larger wins, so the lower
+// index wins exact ties) and their renormalised weights.  One thread.
+__device__ inline void route_topk(const float *logit, int E, int K, int *idx, float *w) {
+    float m = logit[0];
+    for (int e = 1; e < E; ++e) m = fmaxf(m, logit[e]);
+    float p[kMaxExperts];
+    float z = 0.f;
+    for (int e = 0; e < E; ++e) {
+        p[e] = expf(logit[e] - m);
+        z += p[e];
+    }
+    const float inv = 1.f / z;
+    for (int e = 0; e < E; ++e) p[e] *= inv;
+    uint64_t taken = 0;
+    float ps = 0.f;
+    for (int k = 0; k < K; ++k) {
+        int best = -1;
+        for (int e = 0; e < E; ++e)
+            if (!((taken >> e) & 1ull) && (best < 0 || p[e] > p[best])) best = e;
+        taken |= 1ull << best;
+        idx[k] = best;
+        ps += p[best];
+    }
+    for (int k = 0; k < K; ++k) w[k] = p[idx[k]] / ps;
+}
 
 template <typename WT, int NC, bool DENSE, int RIF>
 __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
@@ -351,6 +384,8 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     __shared__ int s_al[kMaxPipeTile];
     __shared__ float s_av[kMaxPipeTile];
     __shared__ int s_n[2];
+    __shared__ float s_logit[kMaxExperts];
+    __shared__ int s_expert;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -364,14 +399,54 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     const int nch = H / CE;
     const size_t pr = (size_t)slot * a.ntiles + tile;
 
+    float xr[NC][CE];
+    const float *xt = a.x + (size_t)tok * H;
+    load_x<WT, NC>(xt, lane, nch, xr);
+
     size_t eoff = 0;
-    if (a.route) eoff = (size_t)a.route[slot] * a.expert_stride;
+    if (a.route) {
+        eoff = (size_t)a.route[slot] * a.expert_stride;
+    } else if (a.wr) {
+        // the token's router: wave w dots expert rows w, w + 8, ...; thread 0
+        // takes the softmax and top-k and picks this slot's expert
+        const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.wr, (uint32_t)a.E * (uint32_t)H * (uint32_t)sizeof(WT));
+        for (int e = wave; e < a.E; e += kWaves) {
+            u32x4 v[NC];
+            const uint32_t base = (uint32_t)e * (uint32_t)H * (uint32_t)sizeof(WT);
+#pragma unroll
+            for (int c0 = 0; c0 < NC; ++c0) {
+                const int c = lane + 64 * c0;
+                v[c0] = ld_buf_stream(rr, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+            }
+            float d = 0.f;
+#pragma unroll
+            for (int c0 = 0; c0 < NC; ++c0) {
+                float f[CE];
+                unpack<WT>(v[c0], f);
+#pragma unroll
+                for (int q = 0; q < CE; ++q) d = fmaf(f[q], xr[c0][q], d);
+            }
+            d = wave_sum(d);
+            if (lane == 0) s_logit[e] = d;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int idx[kMaxTopK];
+            float w[kMaxTopK];
+            route_topk(s_logit, a.E, a.K, idx, w);
+            const int k = slot % a.K;
+            s_expert = idx[k];
+            if (tile == 0) {
+                a.ridx[slot] = idx[k];
+                a.rw[slot] = w[k];
+            }
+        }
+        __syncthreads();
+        eoff = (size_t)s_expert * a.expert_stride;
+    }
     const WT *wg = reinterpret_cast<const WT *>(a.wg) + eoff + (size_t)n0 * H;
     const WT *wu = reinterpret_cast<const WT *>(a.wu) + eoff + (size_t)n0 * H;
     const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff + (size_t)n0 * H;
-
-    float xr[NC][CE];
-    const float *xt = a.x + (size_t)tok * H;
     // buffer resources over the tile's rows (at most 128 rows of 32 KB)
     const uint32_t tbytes = (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT);
     PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H, nch, lane, xr, s_g, s_h, s_on};
@@ -379,7 +454,6 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     // this wave's rows: wave, wave + 8, ...; first two gate rows in flight
     const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
     u32x4 g0[NC], g1[NC], u0[NC], u1[NC];
-    load_x<WT, NC>(xt, lane, nch, xr);
     pw.issue(pw.rg, nrow > 0 ? wave : -1, g0);
     pw.issue(pw.rg, nrow > 1 ? wave + kWaves : -1, g1);
 
@@ -875,30 +949,12 @@ __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, c
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        float m = s_l[0];
-        for (int e = 1; e < E; ++e) m = fmaxf(m, s_l[e]);
-        float p[kMaxExperts];
-        float z = 0.f;
-        for (int e = 0; e < E; ++e) {
-            p[e] = expf(s_l[e] - m);
-            z += p[e];
-        }
-        const float inv = 1.f / z;
-        for (int e = 0; e < E; ++e) p[e] *= inv;
-        uint64_t taken = 0;
         int idx[kMaxTopK];
-        float ps = 0.f;
-        for (int k = 0; k < K; ++k) {
-            int best = -1;
-            for (int e = 0; e < E; ++e)
-                if (!((taken >> e) & 1ull) && (best < 0 || p[e] > p[best])) best = e;
-            taken |= 1ull << best;
-            idx[k] = best;
-            ps += p[best];
-        }
+        float w[kMaxTopK];
+        route_topk(s_l, E, K, idx, w);
         for (int k = 0; k < K; ++k) {
             topk_idx[(size_t)t * K + k] = idx[k];
-            topk_w[(size_t)t * K + k] = p[idx[k]] / ps;
+            topk_w[(size_t)t * K + k] = w[k];
         }
     }
 }
@@ -1078,11 +1134,25 @@ ts_status run_split(const float *x, const void *wg, const void *wu, const void *
 
 // Fused single-token path (the dense comparator, and the default sparse
 // path): one workgroup per tile runs gate, up and down, then ffn_reduce.
+// Router weights and outputs for in-kernel routing (MoE on the pipelined kernel).
+struct RouterFold {
+    const void *wr;
+    int E, K;
+    int32_t *ridx;
+    float *rw;
+};
+
 ts_status run_fused(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
                     size_t expert_stride, ts_dtype dt, bool dense, const SlotPlan &p, float *out,
-                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool pipe) {
+                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool pipe,
+                    const RouterFold *rf = nullptr) {
     const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
     SlotArgs a;
+    a.wr = rf ? rf->wr : nullptr;
+    a.E = rf ? rf->E : 0;
+    a.K = rf ? rf->K : 0;
+    a.ridx = rf ? rf->ridx : nullptr;
+    a.rw = rf ? rf->rw : nullptr;
     a.x = x;
     a.wg = wg;
     a.wu = wu;
@@ -1121,14 +1191,20 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     return run_report(p, a.cnt, a.gseg, a.aseg, a.ntiles, a.tile, stats, ws, st);
 }
 
+// The kernel sequence run_slots picks: the pipelined kernel unless the dense
+// comparator, a tuning knob or a row too wide for it asks for another.
+bool slots_use_pipe(const SlotPlan &p, bool dense) { return !dense && tuned("ffn_path") == 0 && p.nc <= 8; }
+
+// `rf` (pipelined kernel only, route == null) moves the MoE router into it.
 ts_status run_slots(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
                     size_t expert_stride, ts_dtype dt, bool dense, const SlotPlan &p, float *out,
-                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+                    const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st,
+                    const RouterFold *rf = nullptr) {
     const int path = tuned("ffn_path");
     if (dense || path == 2)
         return run_fused(x, wg, wu, wd, route, expert_stride, dt, dense, p, out, slot_w, stats, ws, st, false);
     if (path == 1) return run_split(x, wg, wu, wd, route, expert_stride, dt, p, out, slot_w, stats, ws, st);
-    return run_fused(x, wg, wu, wd, route, expert_stride, dt, false, p, out, slot_w, stats, ws, st, true);
+    return run_fused(x, wg, wu, wd, route, expert_stride, dt, false, p, out, slot_w, stats, ws, st, true, rf);
 }
 
 ts_status check_ffn_args(const float *x, const void *wg, const void *wu, const void *wd, ts_dtype dt, int batch,
@@ -1177,16 +1253,25 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
     const size_t roff = moe_route_offset(batch, hidden, inter, E, K, dt);
     int32_t *ridx = ws_at<int32_t>(ws, roff);
     float *rw = ws_at<float>(ws, roff + align_up256((size_t)batch * K * sizeof(int32_t)));
-    if (dt == TS_F32) launch_router<float>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
-    else launch_router<uint16_t>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
-    s = check_launch("moe_router");
-    if (s != TS_OK) return s;
     BatchPlan bp;
     const size_t estride = (size_t)inter * (size_t)hidden;
-    if (batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp))
+    const bool batched = batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp);
+    // on the pipelined kernel each workgroup routes its own token (no router launch)
+    const bool fold = !batched && slots_use_pipe(p, dense);
+    if (!fold) {
+        if (dt == TS_F32) launch_router<float>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
+        else launch_router<uint16_t>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
+        s = check_launch("moe_router");
+        if (s != TS_OK) return s;
+    }
+    if (batched) {
         s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st, dense);
-    else
+    } else if (fold) {
+        const RouterFold rf{wr, E, K, ridx, rw};
+        s = run_slots(x, wg, wu, wd, nullptr, estride, dt, dense, p, out, rw, stats, ws, st, &rf);
+    } else {
         s = run_slots(x, wg, wu, wd, ridx, estride, dt, dense, p, out, rw, stats, ws, st);
+    }
     if (s != TS_OK) return s;
     if (topk_idx) {
         if (hipMemcpyAsync(topk_idx, ridx, (size_t)batch * K * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
