@@ -47,6 +47,8 @@ def _bind(lib):
     lib.or_ffn.restype = ctypes.c_int
     lib.or_moe.argtypes = [vp, vp, vp, vp, vp, ip, ip, ip, ip, ip, ip, dp, vp, dp, dp, dp, dp, ip]
     lib.or_moe.restype = ctypes.c_int
+    lib.or_ffn_given.argtypes = [vp, vp, vp, vp, ip, ip, ip, ip, vp, vp, ip, dp, vp, vp, ip]
+    lib.or_ffn_given.restype = ctypes.c_int
     lib.or_max_threads.argtypes = []
     lib.or_max_threads.restype = ctypes.c_int
     return lib
@@ -125,6 +127,40 @@ def ffn(x, w_gate, w_up, w_down_t, dtype: int, threads: int = 0, lib=None) -> FF
     if rc != 0:
         raise RuntimeError("or_ffn failed")
     return FFNResult(y=y, g=g, u=u)
+
+
+@dataclass
+class GivenResult:
+    y: np.ndarray          # fp64 [B][H]
+    n_open: np.ndarray     # int32 [B] listed entries with gate > 0
+    n_active: np.ndarray   # int32 [B] listed entries with gate > 0 and up > 0
+
+
+def ffn_given(x, w_gate, w_up, w_down_t, dtype: int, idx, count, threads: int = 0, lib=None) -> GivenResult:
+    """dReLU FFN over given neuron lists in fp64 (list order; entries outside
+    [0, I) skipped): y_t = sum over listed i of max(0, g_i) max(0, u_i) W_down_t[i]."""
+    lib = lib or _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    B, H = x.shape
+    wg, wu, wd = (_weights(w, dtype) for w in (w_gate, w_up, w_down_t))
+    I = wg.shape[0]
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    if idx.ndim == 1:
+        idx = idx[None, :]
+    count = np.ascontiguousarray(count, dtype=np.int32).reshape(-1)
+    if idx.shape[0] != B or count.shape[0] != B:
+        raise ValueError("idx / count must have one row / entry per token")
+    maxc = idx.shape[1]
+    y = np.empty((B, H), np.float64)
+    no = np.empty(B, np.int32)
+    na = np.empty(B, np.int32)
+    rc = lib.or_ffn_given(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), dtype, B, H, I, _ptr(idx), _ptr(count), maxc,
+                          _ptr(y), _ptr(no), _ptr(na), int(threads))
+    if rc != 0:
+        raise RuntimeError("or_ffn_given failed")
+    return GivenResult(y=y, n_open=no, n_active=na)
 
 
 @dataclass

@@ -135,6 +135,83 @@ int or_ffn(const float *x, const void *wg, const void *wu, const void *wdt, int 
 }
 
 /*
+ * The dReLU FFN evaluated over given neuron lists: the interface an
+ * activation predictor drives (section 7 of the paper: the inference engine
+ * evaluates only the neurons predicted active).  For token t only the
+ * entries idx[t][0 .. min(count[t], maxc)) contribute, in list order;
+ * entries outside [0, I) are skipped and a repeated entry counts again:
+ *   y_t[j] = sum over listed i of max(0, g_i) max(0, u_i) W_down_t[i][j].
+ * With a list that holds every neuron whose Combined activation is non-zero
+ * (G_t, or all neurons ascending) this is the dense FFN term for term.
+ *   idx [B][maxc], count [B] int32; y [B][H] fp64 out;
+ *   n_open / n_active [B] (nullable): listed entries with g > 0, and with
+ *   g > 0 and u > 0.
+ * Returns 0, or -1 on bad arguments / allocation failure.
+ */
+int or_ffn_given(const float *x, const void *wg, const void *wu, const void *wdt, int dtype, int B, int H,
+                 int I, const int32_t *idx, const int32_t *count, int maxc, double *y, int32_t *n_open,
+                 int32_t *n_active, int nthreads)
+{
+    if (!x || !wg || !wu || !wdt || !idx || !count || !y || B < 0 || H <= 0 || I < 0 || maxc < 0 ||
+        (dtype != OR_F32 && dtype != OR_BF16))
+        return -1;
+    nthreads = set_threads(nthreads);
+    size_t nL = maxc > 0 ? (size_t)maxc : 1;
+    double *hl = malloc(nL * sizeof *hl);
+    if (!hl)
+        return -1;
+    for (int t = 0; t < B; ++t) {
+        const float *xt = x + (size_t)t * H;
+        const int32_t *lt = idx + (size_t)t * maxc;
+        int n = count[t] < 0 ? 0 : (count[t] > maxc ? maxc : count[t]);
+        int no = 0, na = 0;
+        /* Combined activation of each list entry (0 for skipped entries). */
+        int k;
+#pragma omp parallel for num_threads(nthreads) schedule(static) reduction(+ : no, na)
+        for (k = 0; k < n; ++k) {
+            int i = lt[k];
+            hl[k] = 0.0;
+            if (i < 0 || i >= I)
+                continue;
+            double sg = 0.0, su = 0.0;
+            size_t row = (size_t)i * (size_t)H;
+            for (int j = 0; j < H; ++j) {
+                sg += load_w(wg, dtype, row + j) * (double)xt[j];
+                su += load_w(wu, dtype, row + j) * (double)xt[j];
+            }
+            no += sg > 0.0;
+            na += sg > 0.0 && su > 0.0;
+            hl[k] = (sg > 0.0 && su > 0.0) ? sg * su : 0.0;
+        }
+        if (n_open)
+            n_open[t] = no;
+        if (n_active)
+            n_active[t] = na;
+        /* y[j] = sum over the list, in list order, of h_k * W_down_t[idx_k][j]. */
+        double *yt = y + (size_t)t * H;
+        int nblk = (H + 63) / 64;
+        int b;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+        for (b = 0; b < nblk; ++b) {
+            int j0 = b * 64, j1 = j0 + 64 < H ? j0 + 64 : H;
+            for (int j = j0; j < j1; ++j)
+                yt[j] = 0.0;
+            for (int kk = 0; kk < n; ++kk) {
+                int i = lt[kk];
+                if (i < 0 || i >= I)
+                    continue;
+                double hv = hl[kk];
+                size_t row = (size_t)i * (size_t)H;
+                for (int j = j0; j < j1; ++j)
+                    yt[j] += load_w(wdt, dtype, row + j) * hv;
+            }
+        }
+    }
+    free(hl);
+    return 0;
+}
+
+/*
  * Router of the MoE layer for one token: logits, softmax, top-k, renormalised
  * weights.  logits / probs [E] out; idx [K] ascending-by-rank (rank 0 = largest
  * p); w [K] the renormalised weight of idx[k].

@@ -270,6 +270,108 @@ def pin_moe_special_cases(lib=None):
         assert rm.topk_w[t, 0] >= rm.topk_w[t, 1]
 
 
+# ----------------------------------------------------------------------------
+# Given neuron lists (the activation-predictor interface)
+
+
+def _given_list(rng, I, n, extra_bad=True):
+    """A list of n entries: random neurons with repeats, plus (optionally)
+    entries outside [0, I) that must be skipped."""
+    lst = rng.integers(0, I, size=n).astype(np.int32)
+    if extra_bad and n >= 3:
+        lst[0] = -1
+        lst[n // 2] = I
+        lst[-1] = lst[1]  # a repeat
+    return lst
+
+
+def pin_given_bruteforce(lib=None):
+    """Exact rational sums over the listed neurons (repeats counted, entries
+    outside [0, I) skipped), within the fp64 forward-error bound."""
+    rng = np.random.default_rng(31)
+    for dtype in (synth.F32, synth.BF16):
+        for k, (B, H, I) in enumerate([(1, 4, 6), (2, 8, 16), (3, 5, 9)]):
+            inp = synth.make_ffn(B, H, I, gate_bias=0.2, dtype=dtype, seed=[23, k, dtype])
+            maxc = I + 3
+            idx = np.stack([_given_list(rng, I, maxc) for _ in range(B)])
+            count = np.array([maxc - t for t in range(B)], np.int32)
+            r = oracle.ffn_given(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, idx, count, threads=1, lib=lib)
+            wg, wu, wd = (_as_fractions(w, dtype) for w in (inp.w_gate, inp.w_up, inp.w_down_t))
+            for t in range(B):
+                x = [Fraction(float(v)) for v in inp.x[t]]
+                g, u, h, _, _ = _exact_ffn_token(x, wg, wu, wd)
+                lst = [int(i) for i in idx[t, :count[t]] if 0 <= i < I]
+                eh = []
+                for i in range(I):
+                    eg = gamma(H) * float(sum(abs(wg[i][j] * x[j]) for j in range(H)))
+                    eu = gamma(H) * float(sum(abs(wu[i][j] * x[j]) for j in range(H)))
+                    ag, au = abs(float(g[i])), abs(float(u[i]))
+                    eh.append((ag + eg) * eu + au * eg + U * (ag + eg) * (au + eu))
+                for j in range(H):
+                    y = sum((wd[i][j] * h[i] for i in lst), Fraction(0))
+                    s_abs = sum(abs(float(wd[i][j])) * (abs(float(h[i])) + eh[i]) for i in lst)
+                    bound = gamma(max(len(lst), 1)) * s_abs + sum(abs(float(wd[i][j])) * eh[i] for i in lst)
+                    assert _within(r.y[t, j], y, bound), (dtype, B, H, I, t, j)
+                assert r.n_open[t] == sum(1 for i in lst if g[i] > 0)
+                assert r.n_active[t] == sum(1 for i in lst if g[i] > 0 and u[i] > 0)
+
+
+def pin_given_numpy(lib=None):
+    """Random lists (repeats, out-of-range entries, ragged counts) against a
+    numpy fp64 evaluation of the same sum."""
+    rng = np.random.default_rng(32)
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(3, 96, 300, gate_bias=-0.3, dtype=dtype, seed=33)
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        x = inp.x.astype(np.float64)
+        g = x @ up(inp.w_gate).astype(np.float64).T
+        u = x @ up(inp.w_up).astype(np.float64).T
+        h = np.where((g > 0) & (u > 0), g * u, 0.0)
+        wd = up(inp.w_down_t).astype(np.float64)
+        maxc = 180
+        idx = np.stack([_given_list(rng, 300, maxc) for _ in range(3)])
+        count = np.array([180, 0, 77], np.int32)
+        r = oracle.ffn_given(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, idx, count, lib=lib)
+        for t in range(3):
+            lst = np.array([i for i in idx[t, :count[t]] if 0 <= i < 300], np.int64)
+            y = h[t, lst] @ wd[lst] if len(lst) else np.zeros(96)
+            assert np.allclose(r.y[t], y, rtol=1e-12, atol=1e-12 * max(np.abs(y).max(), 1e-300))
+            assert r.n_open[t] == int((g[t, lst] > 0).sum())
+            assert r.n_active[t] == int(((g[t, lst] > 0) & (u[t, lst] > 0)).sum())
+        assert np.all(r.y[1] == 0.0)
+
+
+def pin_given_exact_sets_bitwise(lib=None):
+    """A list holding every active neuron in ascending order (G_t, or all
+    neurons) reproduces every bit of the dense oracle: the neurons it leaves
+    out contribute exact zeros.  A list missing one active neuron misses
+    exactly that neuron's term."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 128, 400, gate_bias=-0.84, dtype=dtype, seed=34)
+        rd = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, lib=lib)
+        allrows = np.tile(np.arange(400, dtype=np.int32), (2, 1))
+        r = oracle.ffn_given(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, allrows, [400, 400], lib=lib)
+        assert np.array_equal(r.y.view(np.uint64), rd.y.view(np.uint64))
+        assert r.n_open.tolist() == rd.n_gate.tolist() and r.n_active.tolist() == rd.n_active.tolist()
+        G = [rd.gate_set(t) for t in range(2)]
+        idx = np.full((2, 400), -1, np.int32)
+        for t in range(2):
+            idx[t, :len(G[t])] = G[t]
+        r = oracle.ffn_given(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, idx, [len(G[0]), len(G[1])],
+                             lib=lib)
+        assert np.array_equal(r.y.view(np.uint64), rd.y.view(np.uint64))
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        A0 = rd.active_set(0)
+        miss = A0[len(A0) // 2]
+        keep = A0[A0 != miss]
+        idx = np.full((1, 400), 0, np.int32)
+        idx[0, :len(keep)] = keep
+        r = oracle.ffn_given(inp.x[:1], inp.w_gate, inp.w_up, inp.w_down_t, dtype, idx, [len(keep)], lib=lib)
+        term = up(inp.w_down_t)[miss].astype(np.float64) * (rd.g[0, miss] * rd.u[0, miss])
+        assert np.allclose(r.y[0], rd.y[0] - term, rtol=1e-12, atol=1e-12 * np.abs(rd.y[0]).max())
+        assert not np.allclose(r.y[0], rd.y[0], rtol=1e-9, atol=0)
+
+
 ALL_PINS = [pin_ffn_handworked, pin_moe_handworked, pin_ffn_bruteforce, pin_moe_bruteforce,
             pin_ffn_zero_bias, pin_ffn_all_active_numpy, pin_ffn_sets_numpy, pin_ffn_skipzero_bitwise,
-            pin_moe_special_cases]
+            pin_moe_special_cases, pin_given_bruteforce, pin_given_numpy, pin_given_exact_sets_bitwise]

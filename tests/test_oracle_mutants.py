@@ -28,6 +28,12 @@ MUTANTS = {
     "moe_wrong_expert_down": ("const char *base_d = (const char *)wdt + (size_t)e * expert_bytes;",
                               "const char *base_d = (const char *)wdt;"),
     "moe_rank_weight_swap": ("yt[j] += w[rank] * ye[j];", "yt[j] += w[K - 1 - rank] * ye[j];"),
+    "given_gate_only_relu": ("hl[k] = (sg > 0.0 && su > 0.0) ? sg * su : 0.0;", "hl[k] = (sg > 0.0) ? sg * su : 0.0;"),
+    "given_count_ignored": ("int n = count[t] < 0 ? 0 : (count[t] > maxc ? maxc : count[t]);", "int n = maxc;"),
+    "given_down_list_position": ("double hv = hl[kk];\n                size_t row = (size_t)i * (size_t)H;",
+                                 "double hv = hl[kk];\n                size_t row = (size_t)kk * (size_t)H;"),
+    "given_repeat_dropped": ("for (int kk = 0; kk < n; ++kk) {\n                int i = lt[kk];\n                if (i < 0 || i >= I)\n                    continue;",
+                             "for (int kk = 0; kk < n; ++kk) {\n                int i = lt[kk];\n                if (i < 0 || i >= I || (kk > 0 && lt[kk - 1] == i) || (kk > 1 && lt[kk - 2] == i))\n                    continue;"),
 }
 
 
