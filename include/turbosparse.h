@@ -121,6 +121,38 @@ ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, con
                        ts_dtype wdtype, int batch, int hidden, int inter, float *out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* Workspace bytes for ts_ffn_sparse_given (0 if out of range). */
+size_t ts_ffn_given_workspace_bytes(int batch, int hidden, int inter, int max_count, ts_dtype wdtype);
+
+/*
+ * Sparse dReLU FFN over externally supplied neuron lists: the interface an
+ * activation predictor drives (section 7 of the paper: the inference engine
+ * evaluates only the neurons a predictor marks active, so the gate
+ * projection of the other neurons is never read).  For token t only the
+ * entries idx[t][0 .. min(count[t], max_count)) are evaluated, in any
+ * order: their W_gate rows are read, the W_up rows of those whose gate is
+ * positive, and the W_down_t rows of those whose Combined activation is
+ * non-zero.  Entries outside [0, inter) are skipped; a repeated entry
+ * contributes again.  A list that holds every neuron of G_t (for instance
+ * the gate_idx report of ts_ffn_sparse) gives the ts_ffn_sparse result up
+ * to fp32 summation order; a list that misses active neurons leaves their
+ * terms out (the predictor's approximation).
+ *   idx   device int32 [batch][max_count]; count device int32 [batch]
+ *         (values below 0 count as 0, above max_count as max_count);
+ *   stats nullable; only n_gate (listed entries with a positive gate) and
+ *         n_active (listed entries with a non-zero Combined activation)
+ *         are served, the other stats fields must be NULL
+ *         (TS_ERR_UNSUPPORTED otherwise);
+ *   other arguments and constraints as ts_ffn_sparse, plus
+ *   1 <= max_count <= 2^24, idx and count 4-byte aligned, and rows of at
+ *   most 512 16-byte chunks (hidden <= 4096 for TS_BF16, <= 2048 for
+ *   TS_F32; TS_ERR_UNSUPPORTED otherwise).
+ */
+ts_status ts_ffn_sparse_given(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                              ts_dtype wdtype, int batch, int hidden, int inter, const int32_t *idx,
+                              const int32_t *count, int max_count, float *out, const ts_ffn_stats *stats,
+                              void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes for ts_moe_sparse / ts_moe_dense (0 if out of range). */
 size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, int top_k,
                               ts_dtype wdtype);

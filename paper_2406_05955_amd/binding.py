@@ -20,7 +20,8 @@ TS_BF16 = 1
 STATUS = {0: "TS_OK", 1: "TS_ERR_NULL", 2: "TS_ERR_SHAPE", 3: "TS_ERR_DTYPE", 4: "TS_ERR_ALIGN",
           5: "TS_ERR_WORKSPACE", 6: "TS_ERR_HIP", 7: "TS_ERR_UNSUPPORTED"}
 
-EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_dense", "ts_moe_workspace_bytes", "ts_moe_sparse",
+EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_dense", "ts_ffn_given_workspace_bytes",
+            "ts_ffn_sparse_given", "ts_moe_workspace_bytes", "ts_moe_sparse",
             "ts_moe_dense", "ts_status_str", "ts_last_error", "ts_version", "ts_prof_enable", "ts_prof_reset",
             "ts_prof_read", "ts_probe_read", "ts_probe_copy", "ts_tune_set"]
 
@@ -49,6 +50,10 @@ def _load() -> ctypes.CDLL:
     lib.ts_ffn_sparse.restype = st
     lib.ts_ffn_dense.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, sz, vp]
     lib.ts_ffn_dense.restype = st
+    lib.ts_ffn_given_workspace_bytes.argtypes = [i, i, i, i, i]
+    lib.ts_ffn_given_workspace_bytes.restype = sz
+    lib.ts_ffn_sparse_given.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, i, vp, vp, vp, sz, vp]
+    lib.ts_ffn_sparse_given.restype = st
     lib.ts_moe_workspace_bytes.argtypes = [i, i, i, i, i, i]
     lib.ts_moe_workspace_bytes.restype = sz
     lib.ts_moe_sparse.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, vp, vp, vp, vp, sz, vp]
@@ -113,6 +118,10 @@ def ffn_workspace_bytes(batch: int, hidden: int, inter: int, wdtype: int) -> int
     return int(lib.ts_ffn_workspace_bytes(batch, hidden, inter, wdtype))
 
 
+def ffn_given_workspace_bytes(batch: int, hidden: int, inter: int, max_count: int, wdtype: int) -> int:
+    return int(lib.ts_ffn_given_workspace_bytes(batch, hidden, inter, max_count, wdtype))
+
+
 def moe_workspace_bytes(batch: int, hidden: int, inter: int, n_experts: int, top_k: int, wdtype: int) -> int:
     return int(lib.ts_moe_workspace_bytes(batch, hidden, inter, n_experts, top_k, wdtype))
 
@@ -170,6 +179,34 @@ def ffn_dense(x, w_gate, w_up, w_down_t, out=None, ws=None, stream=None):
                             ws.numel(), _stream(stream))
     _check(code, "ts_ffn_dense")
     return out
+
+
+def ffn_sparse_given(x, w_gate, w_up, w_down_t, idx, count, out=None, stats: bool = False, ws=None, stream=None):
+    """ts_ffn_sparse_given: the FFN over given neuron lists.  idx int32
+    [B][max_count], count int32 [B] (device tensors).  Returns out, or (out,
+    {"n_gate", "n_active"}) with stats=True."""
+    _need_cuda(x, w_gate, w_up, w_down_t, out, idx, count)
+    B, H = x.shape
+    I = w_gate.shape[0]
+    dt = wdtype_of(w_gate)
+    if idx.dim() != 2 or idx.shape[0] != B or count.numel() != B:
+        raise ValueError("idx must be [batch][max_count] and count [batch]")
+    if idx.dtype != torch.int32 or count.dtype != torch.int32:
+        raise TypeError("idx and count must be int32")
+    maxc = idx.shape[1]
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    ws = _workspace(ffn_given_workspace_bytes(B, H, I, maxc, dt), x.device, ws)
+    d = st = None
+    if stats:
+        d = {"n_gate": torch.empty(B, dtype=torch.int32, device=x.device),
+             "n_active": torch.empty(B, dtype=torch.int32, device=x.device)}
+        st = ffn_stats_t(_ptr(d["n_gate"]), _ptr(d["n_active"]), None, None, None)
+    code = lib.ts_ffn_sparse_given(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(idx),
+                                   _ptr(count), maxc, _ptr(out), ctypes.byref(st) if st is not None else None,
+                                   _ptr(ws), ws.numel(), _stream(stream))
+    _check(code, "ts_ffn_sparse_given")
+    return (out, d) if d is not None else out
 
 
 def moe_sparse(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, stats: bool = False, ws=None,

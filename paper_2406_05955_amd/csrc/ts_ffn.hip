@@ -553,6 +553,238 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Given-list kernel (ts_ffn_sparse_given): the pipelined kernel's per-wave
+// gate / up stream and down axpy, over a chunk of a token's neuron list
+// instead of a tile of consecutive neurons.  The chunk's entries are staged
+// in LDS (entries outside [0, inter) become -1); each row load goes through
+// a buffer resource over that one row, an unused slot or a skipped entry
+// loads at an out-of-range offset (zeros, no traffic).  One partial output
+// row per (token, chunk), summed by ffn_reduce in chunk order.
+
+struct GivenArgs {
+    const float *x;
+    const void *wg, *wu, *wd;
+    const int32_t *idx;      // [tokens][maxc]
+    const int32_t *count;    // [tokens]
+    int H, I, maxc, chunk, nchunks;
+    float *partial;          // [tokens][nchunks][H]
+    int32_t *cnt;            // [tokens][nchunks][2] listed entries with gate > 0 / non-zero Combined
+};
+
+template <typename WT, int NC>
+struct GivenWave {
+    static constexpr int CE = WTraits<WT>::CE;
+    const WT *wg, *wu;
+    const float *xt;        // any valid address: base of the empty resource of an unused slot
+    const int *s_row;       // chunk entry -> neuron (-1: skipped)
+    int H, nch, lane;
+    float (&xr)[NC][CE];
+    float *s_g, *s_h;
+    int *s_on;
+
+    // Loads of chunk entry r (r < 0 or a skipped entry: zeros) from matrix `w`.
+    __device__ void issue(const WT *w, int r, u32x4 (&v)[NC]) {
+        // (wave-uniform, but derived from the thread index: made provably
+        // uniform so the resource stays in scalar registers)
+        const int n = __builtin_amdgcn_readfirstlane(r >= 0 ? s_row[r >= 0 ? r : 0] : -1);
+        const __amdgpu_buffer_rsrc_t rs =
+            make_rsrc(n >= 0 ? static_cast<const void *>(w + (size_t)(n >= 0 ? n : 0) * H) : xt,
+                      n >= 0 ? (uint32_t)H * (uint32_t)sizeof(WT) : 0u);
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) {
+            const int c = lane + 64 * c0;
+            v[c0] = ld_buf_stream(rs, (n >= 0 && c < nch) ? (uint32_t)c * 16u : kOutOfRange);
+        }
+    }
+    __device__ float dot(const u32x4 (&v)[NC]) {
+        float d = 0.f;
+#pragma unroll
+        for (int c0 = 0; c0 < NC; ++c0) {
+            float f[CE];
+            unpack<WT>(v[c0], f);
+#pragma unroll
+            for (int e = 0; e < CE; ++e) d = fmaf(f[e], xr[c0][e], d);
+        }
+        return wave_sum(d);
+    }
+    // As PipeWave::step, over chunk entries.
+    __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC],
+                         u32x4 (&uprev)[NC], int &prev_row) {
+        const float g = dot(gcur);
+        const bool open = valid && g > 0.f;
+        issue(wu, open ? row : -1, ucur);
+        issue(wg, next2, gcur);
+        if (lane == 0 && valid) {
+            s_g[row] = g;
+            s_on[row] = 0;
+            s_h[row] = 0.f;
+        }
+        if (prev_row >= 0) {
+            const float u = dot(uprev);
+            if (lane == 0 && u > 0.f) {
+                s_on[prev_row] = 1;
+                s_h[prev_row] = s_g[prev_row] * u;
+            }
+        }
+        prev_row = open ? row : -1;
+    }
+};
+
+template <typename WT, int NC, int MR>
+__global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
+    constexpr int CE = WTraits<WT>::CE;
+    constexpr int NCD = (NC * 64 + kThreads - 1) / kThreads;
+
+    __shared__ int s_row[kMaxPipeTile];
+    __shared__ float s_g[kMaxPipeTile];
+    __shared__ float s_h[kMaxPipeTile];
+    __shared__ int s_on[kMaxPipeTile];
+    __shared__ int s_al[kMaxPipeTile];
+    __shared__ float s_av[kMaxPipeTile];
+    __shared__ int s_n[2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int chunk = blockIdx.x % a.nchunks;
+    const int tok = blockIdx.x / a.nchunks;
+    const int H = a.H;
+    const int nch = H / CE;
+    const int n_list = min(max(a.count[tok], 0), a.maxc);
+    const int e0 = chunk * a.chunk;
+    const int nt = max(0, min(a.chunk, n_list - e0));
+    const size_t pr = (size_t)tok * a.nchunks + chunk;
+
+    float xr[NC][CE];
+    const float *xt = a.x + (size_t)tok * H;
+    load_x<WT, NC>(xt, lane, nch, xr);
+    for (int r = tid; r < nt; r += kThreads) {
+        const int v = a.idx[(size_t)tok * a.maxc + e0 + r];
+        s_row[r] = (v >= 0 && v < a.I) ? v : -1;
+    }
+    __syncthreads();
+
+    const WT *wg = reinterpret_cast<const WT *>(a.wg);
+    const WT *wu = reinterpret_cast<const WT *>(a.wu);
+    const WT *wd = reinterpret_cast<const WT *>(a.wd);
+    GivenWave<WT, NC> gw{wg, wu, xt, s_row, H, nch, lane, xr, s_g, s_h, s_on};
+
+    // this wave's entries: wave, wave + 8, ...; first two gate rows in flight
+    const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
+    u32x4 g0[NC], g1[NC], u0[NC], u1[NC];
+    gw.issue(wg, nrow > 0 ? wave : -1, g0);
+    gw.issue(wg, nrow > 1 ? wave + kWaves : -1, g1);
+    int prev = -1;
+#pragma unroll
+    for (int i = 0; i < MR; i += 2) {
+        const int r = wave + kWaves * i;
+        gw.step(r, i < nrow, i + 2 < nrow ? r + 2 * kWaves : -1, g0, u0, u1, prev);
+        gw.step(r + kWaves, i + 1 < nrow, i + 3 < nrow ? r + 3 * kWaves : -1, g1, u1, u0, prev);
+    }
+    if (prev >= 0) {
+        const float u = gw.dot(u1);
+        if (lane == 0 && u > 0.f) {
+            s_on[prev] = 1;
+            s_h[prev] = s_g[prev] * u;
+        }
+    }
+    __syncthreads();
+
+    // ---- ballots: entries with an open gate (count) and non-zero Combined ----
+    if (wave == 0) {
+        int ng = 0, na0 = 0;
+        for (int h = 0; h < kMaxPipeTile / 64; ++h) {
+            const int r = lane + 64 * h;
+            const bool in = r < nt && s_row[r] >= 0;
+            const uint64_t mg = __ballot(in && s_g[r] > 0.f);
+            const bool pa = in && s_on[r];
+            const uint64_t ma = __ballot(pa);
+            if (pa) {
+                const int pos = na0 + lane_prefix(ma, lane);
+                s_al[pos] = r;
+                s_av[pos] = s_h[r];
+            }
+            ng += __popcll(mg);
+            na0 += __popcll(ma);
+        }
+        if (lane == 0) {
+            s_n[0] = ng;
+            s_n[1] = na0;
+        }
+    }
+    __syncthreads();
+    const int na = s_n[1];
+
+    // ---- down: axpy over the W_down_t rows of the non-zero entries ----------
+    float acc[NCD][CE];
+#pragma unroll
+    for (int kd = 0; kd < NCD; ++kd)
+#pragma unroll
+        for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
+    for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
+        u32x4 v[kDownUnroll][NCD];
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const int aa = a0 + u;
+            const int n = __builtin_amdgcn_readfirstlane(aa < na ? s_row[s_al[aa < na ? aa : 0]] : -1);
+            const __amdgpu_buffer_rsrc_t rs =
+                make_rsrc(n >= 0 ? static_cast<const void *>(wd + (size_t)(n >= 0 ? n : 0) * H) : xt,
+                          n >= 0 ? (uint32_t)H * (uint32_t)sizeof(WT) : 0u);
+#pragma unroll
+            for (int kd = 0; kd < NCD; ++kd) {
+                const int c = tid + kThreads * kd;
+                v[u][kd] = ld_buf_stream(rs, (n >= 0 && c < nch) ? (uint32_t)c * 16u : kOutOfRange);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
+#pragma unroll
+            for (int kd = 0; kd < NCD; ++kd) {
+                float f[CE];
+                unpack<WT>(v[u][kd], f);
+#pragma unroll
+                for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
+            }
+        }
+    }
+    float *prow = a.partial + pr * H;
+#pragma unroll
+    for (int kd = 0; kd < NCD; ++kd) {
+        const int c = tid + kThreads * kd;
+        if (c < nch) {
+#pragma unroll
+            for (int e = 0; e < CE; e += 4)
+                *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
+                    f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
+        }
+    }
+    if (tid == 0) {
+        a.cnt[pr * 2] = s_n[0];
+        a.cnt[pr * 2 + 1] = na;
+    }
+}
+
+// Per token: the chunks' counts summed (n_gate, n_active of the report).
+__global__ __launch_bounds__(64) void given_counts(const int32_t *__restrict__ cnt, int nchunks,
+                                                   int32_t *__restrict__ n_gate, int32_t *__restrict__ n_active) {
+    const int t = blockIdx.x;
+    int g = 0, a = 0;
+    for (int c = threadIdx.x; c < nchunks; c += 64) {
+        g += cnt[((size_t)t * nchunks + c) * 2];
+        a += cnt[((size_t)t * nchunks + c) * 2 + 1];
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        g += __shfl_xor(g, o, 64);
+        a += __shfl_xor(a, o, 64);
+    }
+    if (threadIdx.x == 0) {
+        if (n_gate) n_gate[t] = g;
+        if (n_active) n_active[t] = a;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Split path, kernel 1: gate GEMV + ReLU + ballot compaction and the gathered
 // up rows for a tile of `tile` neurons per 4-wave workgroup.  Output per tile:
 // |G|, |A|, the ascending A segment with its Combined values (and the G
@@ -1017,6 +1249,25 @@ void launch_pipe(int nc, int tile, dim3 grid, hipStream_t st, const SlotArgs &a)
 }
 
 template <typename WT, int NC>
+void launch_given_mr(int chunk, dim3 grid, hipStream_t st, const GivenArgs &a) {
+    const int rows = (chunk + kWaves - 1) / kWaves;
+    if (rows <= 2) launch("ffn_given", ffn_given<WT, NC, 2>, grid, dim3(kThreads), st, a);
+    else if (rows <= 4) launch("ffn_given", ffn_given<WT, NC, 4>, grid, dim3(kThreads), st, a);
+    else if (rows <= 8) launch("ffn_given", ffn_given<WT, NC, 8>, grid, dim3(kThreads), st, a);
+    else launch("ffn_given", ffn_given<WT, NC, 16>, grid, dim3(kThreads), st, a);
+}
+
+template <typename WT>
+void launch_given(int nc, int chunk, dim3 grid, hipStream_t st, const GivenArgs &a) {
+    switch (nc) {
+    case 1: launch_given_mr<WT, 1>(chunk, grid, st, a); break;
+    case 2: launch_given_mr<WT, 2>(chunk, grid, st, a); break;
+    case 4: launch_given_mr<WT, 4>(chunk, grid, st, a); break;
+    default: launch_given_mr<WT, 8>(chunk, grid, st, a); break;
+    }
+}
+
+template <typename WT, int NC>
 void launch_gate_up_rif(int rif, dim3 grid, hipStream_t st, const GateArgs &a) {
     if (rif == 1) launch("ffn_gate_up", ffn_gate_up<WT, NC, 1>, grid, dim3(kGateThreads), st, a);
     else launch("ffn_gate_up", ffn_gate_up<WT, NC, 2>, grid, dim3(kGateThreads), st, a);
@@ -1340,6 +1591,57 @@ ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, con
         return TS_OK;
     }
     return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, true, p, out, nullptr, nullptr, ws, st);
+}
+
+ts_status ts_ffn_sparse_given(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                              ts_dtype wdtype, int batch, int hidden, int inter, const int32_t *idx,
+                              const int32_t *count, int max_count, float *out, const ts_ffn_stats *stats,
+                              void *ws, size_t ws_bytes, void *stream) {
+    ts_status s = ts::check_dims(batch, hidden, inter, wdtype);
+    if (s != TS_OK) return s;
+    if (!x || !w_gate || !w_up || !w_down_t || !out || !idx || !count) return TS_ERR_NULL;
+    if (!ts::aligned16(x) || !ts::aligned16(w_gate) || !ts::aligned16(w_up) || !ts::aligned16(w_down_t) ||
+        !ts::aligned16(out) || !ts::aligned4(idx) || !ts::aligned4(count))
+        return TS_ERR_ALIGN;
+    s = ts::check_stats(stats);
+    if (s != TS_OK) return s;
+    if (stats && (stats->gate_idx || stats->active_idx || stats->n_union)) return TS_ERR_UNSUPPORTED;
+    ts::GivenPlan p;
+    if (!ts::plan_given(batch, hidden, inter, max_count, wdtype, &p)) return TS_ERR_SHAPE;
+    if (p.nc > 8) return TS_ERR_UNSUPPORTED;
+    if (!ws || ws_bytes < p.total) return TS_ERR_WORKSPACE;
+    if (!ts::aligned16(ws)) return TS_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    ts::GivenArgs a;
+    a.x = x;
+    a.wg = w_gate;
+    a.wu = w_up;
+    a.wd = w_down_t;
+    a.idx = idx;
+    a.count = count;
+    a.H = hidden;
+    a.I = inter;
+    a.maxc = max_count;
+    a.chunk = p.chunk;
+    a.nchunks = p.nchunks;
+    a.partial = ts::ws_at<float>(ws, p.off_partial);
+    a.cnt = ts::ws_at<int32_t>(ws, p.off_cnt);
+    const dim3 grid((unsigned)(batch * p.nchunks));
+    if (wdtype == TS_F32) ts::launch_given<float>(p.nc, p.chunk, grid, st, a);
+    else ts::launch_given<uint16_t>(p.nc, p.chunk, grid, st, a);
+    s = ts::check_launch("ffn_given");
+    if (s != TS_OK) return s;
+    const dim3 rgrid((unsigned)((hidden / 4 + ts::kRedCols4 - 1) / ts::kRedCols4), (unsigned)batch);
+    ts::launch("ffn_reduce", ts::ffn_reduce, rgrid, dim3(256), st, static_cast<const float *>(a.partial), p.nchunks,
+               hidden, 1, static_cast<const float *>(nullptr), out);
+    s = ts::check_launch("ffn_reduce");
+    if (s != TS_OK) return s;
+    if (stats && (stats->n_gate || stats->n_active)) {
+        ts::launch("ffn_stats", ts::given_counts, dim3((unsigned)batch), dim3(64), st,
+                   static_cast<const int32_t *>(a.cnt), p.nchunks, stats->n_gate, stats->n_active);
+        s = ts::check_launch("given_counts");
+    }
+    return s;
 }
 
 ts_status ts_moe_sparse(const float *x, const void *w_router, const void *w_gate, const void *w_up,

@@ -207,6 +207,44 @@ bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtyp
     return true;
 }
 
+// Chunk of list entries per workgroup: enough workgroups for one per compute
+// unit over the whole batch, a multiple of 8 (rows per wave x 8 waves), at
+// most 128; the ffn_tile knob overrides.
+bool plan_given(int batch, int hidden, int inter, int max_count, ts_dtype dt, GivenPlan *p) {
+    if (check_dims(batch, hidden, inter, dt) != TS_OK || max_count < 1 || max_count > kMaxGivenList) return false;
+    GivenPlan q;
+    q.batch = batch;
+    q.hidden = hidden;
+    q.inter = inter;
+    q.maxc = max_count;
+    q.nch = hidden / (16 / esize(dt));
+    const int need = (q.nch + 63) / 64;
+    q.nc = 1;
+    while (q.nc < need) q.nc <<= 1;
+    int t = tuned_tile();
+    if (t <= 0) {
+        long long per = ((long long)max_count * batch + kTargetTiles - 1) / kTargetTiles;
+        per = (per + 7) / 8 * 8;
+        t = (int)std::max(8LL, std::min((long long)kMaxPipeTile, per));
+    }
+    q.chunk = std::min(t, kMaxPipeTile);
+    q.nchunks = (max_count + q.chunk - 1) / q.chunk;
+    const size_t rows = (size_t)batch * q.nchunks;
+    size_t off = 0;
+    q.off_partial = off;  // [batch][nchunks][hidden] partial output rows
+    off = align256(off + rows * (size_t)hidden * sizeof(float));
+    q.off_cnt = off;      // [batch][nchunks][2] listed entries with gate > 0 / non-zero Combined
+    off = align256(off + rows * 2 * sizeof(int32_t));
+    q.total = off;
+    *p = q;
+    return true;
+}
+
+size_t given_ws_bytes(int batch, int hidden, int inter, int max_count, ts_dtype dt) {
+    GivenPlan g;
+    return plan_given(batch, hidden, inter, max_count, dt, &g) ? g.total : 0;
+}
+
 // Both the single-token and the batched plans must fit (the entry points
 // pick a path at call time, and the tuning knobs can move the choice).
 size_t ffn_ws_bytes(int batch, int hidden, int inter, ts_dtype dt) {
@@ -256,6 +294,10 @@ const char *ts_status_str(ts_status s) {
 
 size_t ts_ffn_workspace_bytes(int batch, int hidden, int inter, ts_dtype wdtype) {
     return ts::ffn_ws_bytes(batch, hidden, inter, wdtype);
+}
+
+size_t ts_ffn_given_workspace_bytes(int batch, int hidden, int inter, int max_count, ts_dtype wdtype) {
+    return ts::given_ws_bytes(batch, hidden, inter, max_count, wdtype);
 }
 
 size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, int top_k, ts_dtype wdtype) {

@@ -78,6 +78,18 @@ struct BatchPlan {
     size_t total = 0;
 };
 
+// Given-list path (ts_ffn_sparse_given): each token's list is cut into
+// chunks of `chunk` entries, one pipelined workgroup per (token, chunk).
+constexpr int kMaxGivenList = 1 << 24;  // entries per token list
+struct GivenPlan {
+    int batch = 0, hidden = 0, inter = 0, maxc = 0;
+    int nch = 0, nc = 0;     // 16-byte chunks per row, per lane (power of two)
+    int chunk = 0, nchunks = 0;
+    size_t off_partial = 0, off_cnt = 0, total = 0;
+};
+bool plan_given(int batch, int hidden, int inter, int max_count, ts_dtype dt, GivenPlan *p);
+size_t given_ws_bytes(int batch, int hidden, int inter, int max_count, ts_dtype dt);
+
 int tuned_tile();
 int choose_tile(int inter, int slots, int cap);
 int tuned(const char *key);

@@ -114,3 +114,36 @@ def test_tune_checks():
     small = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
     assert ts.lib.ts_tune_set(b"ffn_tile", 0) == OK
     assert ts.ffn_workspace_bytes(1, 4096, 14336, 1) < small
+
+
+def test_given_checks():
+    f = ts.lib.ts_ffn_sparse_given
+
+    def call(x=A, dt=1, B=1, H=4096, I=14336, idx=A, cnt=A, maxc=3000, out=A, stats=None, ws=A, wsb=1 << 40):
+        return f(x, A, A, A, dt, B, H, I, idx, cnt, maxc, out, stats, ws, wsb, None)
+    need = ts.ffn_given_workspace_bytes(1, 4096, 14336, 3000, 1)
+    assert need > 0
+    assert ts.ffn_given_workspace_bytes(1, 4096, 14336, 0, 1) == 0
+    assert ts.ffn_given_workspace_bytes(2, 4096, 14336, 3000, 1) > need
+    assert call(maxc=0) == SHAPE
+    assert call(maxc=(1 << 24) + 1) == SHAPE
+    assert call(B=0) == SHAPE
+    assert call(dt=5) == DTYPE
+    assert call(idx=None) == NULL
+    assert call(cnt=None) == NULL
+    assert call(x=None) == NULL
+    assert call(idx=A + 2) == ALIGN
+    assert call(cnt=A + 1) == ALIGN
+    assert call(out=A + 4) == ALIGN
+    assert call(wsb=need - 1) == WS
+    assert call(ws=None) == WS
+    # rows wider than the pipelined kernel serves (bf16 hidden 8192, fp32 hidden 4096)
+    assert call(H=8192) == UNSUP
+    assert call(H=4096, dt=0) == UNSUP
+    # only the counts of the activity report are served
+    st = ts.ffn_stats_t(None, None, A, None, None)
+    assert call(stats=ctypes.byref(st)) == UNSUP
+    st = ts.ffn_stats_t(None, None, None, None, A)
+    assert call(stats=ctypes.byref(st)) == UNSUP
+    st = ts.ffn_stats_t(A + 2, None, None, None, None)
+    assert call(stats=ctypes.byref(st)) == ALIGN
