@@ -17,7 +17,9 @@ per-launch HIP events, and the fp64 oracle
 timed on the host cores as a CPU baseline.
 
 Other workloads (--workload): sweep (gate bias for 50/75/90/95/99% sparsity),
-moe (Mixtral-shaped top-2 MoE layer, batch 1 and 16), batch (batch 8 and 32).
+moe (Mixtral-shaped top-2 MoE layer, batch 1 and 16), batch (batch 8 and 32),
+given (predictor mode: each layer called with its exact gate set as the
+neuron list).
 """
 from __future__ import annotations
 
@@ -45,7 +47,7 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=32)
-    ap.add_argument("--workload", default="mistral", choices=["mistral", "sweep", "moe", "batch", "all"])
+    ap.add_argument("--workload", default="mistral", choices=["mistral", "sweep", "moe", "batch", "given", "all"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle CPU-baseline leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -296,6 +298,61 @@ def run_sweep(args, ts, synth, torch):
     return out
 
 
+def run_given_workload(args, ts, synth, torch):
+    """Predictor mode on the Mistral-shaped stack, batch 1: each layer is
+    called with an externally supplied neuron list (ts_ffn_sparse_given), here
+    the exact gate set G of the layer's token (what a perfect activation
+    predictor would return), so W_gate is read only for the listed rows.
+    Points at 90% and 99% zero Combined activations."""
+    out = []
+    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
+    for s in (0.90, 0.99):
+        b = synth.gate_bias_for_combined_sparsity(s)
+        stack = Stack(ts, synth, L, 1, H, I, gate_bias=b, seed=3)
+        d = stack.data
+        lists, counts = [], []
+        for l in range(L):
+            _, st = ts.ffn_sparse(d["x"][l], d["w_gate"][l], d["w_up"][l], d["w_down_t"][l], stats=True)
+            torch.cuda.synchronize()
+            ng, na = int(st["n_gate"][0]), int(st["n_active"][0])
+            lists.append((st["gate_idx"][:, :max(ng, 1)].contiguous(),
+                          torch.tensor([ng], dtype=torch.int32, device="cuda")))
+            counts.append((ng, na))
+        maxc = max(int(li.shape[1]) for li, _ in lists)
+        wsb = ts.ffn_given_workspace_bytes(1, H, I, maxc, ts.TS_BF16)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        f = ts.lib.ts_ffn_sparse_given
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        vp = ctypes.c_void_p
+        argl = [(vp(d["x"][l].data_ptr()), vp(d["w_gate"][l].data_ptr()), vp(d["w_up"][l].data_ptr()),
+                 vp(d["w_down_t"][l].data_ptr()), ts.TS_BF16, 1, H, I, vp(lists[l][0].data_ptr()),
+                 vp(lists[l][1].data_ptr()), int(lists[l][0].shape[1]), vp(stack.out[l].data_ptr()))
+                for l in range(L)]
+
+        def step_given():
+            for a in argl:
+                rc = f(*a, None, ws.data_ptr(), wsb, stream)
+                if rc:
+                    raise RuntimeError(f"ts_ffn_sparse_given -> {rc}")
+        tg = timed(torch, step_given, args.steps, args.warmup)
+        tsp = timed(torch, stack.step_sparse, args.steps, args.warmup)
+        td = timed(torch, stack.step_dense, args.steps, args.warmup)
+        n, ms = kernel_avg_ms(ts, torch, step_given, max(3, args.steps // 3), "ffn_given")
+        # bytes: W_gate, W_up rows of the listed (= open) neurons, W_down_t rows of A, x and out
+        alg = sum(2 * H * (2 * ng + na) + 8 * H for ng, na in counts) / L
+        dense = 3 * 2 * H * I + 8 * H
+        out.append({"workload": "mistral7b_ffn_stack_bf16_b1_given_gate_set", "target_sparsity": s,
+                    "measured_sparsity": 1 - sum(c[1] for c in counts) / (L * I),
+                    "given_tokens_per_s_layer": L / tg, "sparse_tokens_per_s_layer": L / tsp,
+                    "dense_tokens_per_s_layer": L / td, "speedup_vs_dense": td / tg,
+                    "byte_bound_speedup": dense / alg, "literal_target_0.6_over_1_minus_s": 0.6 / (1 - s),
+                    "touched_bytes_per_layer": alg, "given_GBps_touched": alg / (tg / L) / 1e9,
+                    "ffn_given_us": ms * 1e3 if n else None})
+        del stack, lists, ws
+        torch.cuda.empty_cache()
+    return out
+
+
 def batch_kernels(ts, torch, fn, steps):
     res = {}
     for k in ("batch_dispatch", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
@@ -452,7 +509,7 @@ def main():
     if args.workload == "mistral":
         print(json.dumps(run_mistral(args, ts, synth, torch)), flush=True)
         return
-    runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload}
+    runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload, "given": run_given_workload}
     names = list(runs) if args.workload == "all" else [args.workload]
     for n in names:
         for r in runs[n](args, ts, synth, torch):

@@ -130,8 +130,9 @@ size_t ts_ffn_given_workspace_bytes(int batch, int hidden, int inter, int max_co
  * evaluates only the neurons a predictor marks active, so the gate
  * projection of the other neurons is never read).  For token t only the
  * entries idx[t][0 .. min(count[t], max_count)) are evaluated, in any
- * order: their W_gate rows are read, the W_up rows of those whose gate is
- * positive, and the W_down_t rows of those whose Combined activation is
+ * order: their W_gate and W_up rows are read (together: a listed neuron is
+ * predicted active, so the up row is not held back until the gate's sign is
+ * known), and the W_down_t rows of those whose Combined activation is
  * non-zero.  Entries outside [0, inter) are skipped; a repeated entry
  * contributes again.  A list that holds every neuron of G_t (for instance
  * the gate_idx report of ts_ffn_sparse) gives the ts_ffn_sparse result up

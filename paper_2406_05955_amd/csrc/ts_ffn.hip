@@ -553,9 +553,10 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Given-list kernel (ts_ffn_sparse_given): the pipelined kernel's per-wave
-// gate / up stream and down axpy, over a chunk of a token's neuron list
-// instead of a tile of consecutive neurons.  The chunk's entries are staged
+// Given-list kernel (ts_ffn_sparse_given): per-wave gate / up stream and
+// down axpy as in the pipelined kernel, over a chunk of a token's neuron
+// list instead of a tile of consecutive neurons; a listed neuron's W_gate
+// and W_up rows are requested together.  The chunk's entries are staged
 // in LDS (entries outside [0, inter) become -1); each row load goes through
 // a buffer resource over that one row, an unused slot or a skipped entry
 // loads at an out-of-range offset (zeros, no traffic).  One partial output
@@ -607,26 +608,22 @@ struct GivenWave {
         }
         return wave_sum(d);
     }
-    // As PipeWave::step, over chunk entries.
-    __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC],
-                         u32x4 (&uprev)[NC], int &prev_row) {
+    // One entry: its gate and up dots from gcur / ucur (both rows were
+    // requested together, two entries ahead), then the rows of the entry
+    // two ahead into the same registers.  A listed neuron is predicted
+    // active, so its W_up row is read without waiting for the gate's sign:
+    // one dependent memory round trip per entry instead of two.
+    __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC]) {
         const float g = dot(gcur);
-        const bool open = valid && g > 0.f;
-        issue(wu, open ? row : -1, ucur);
+        const float u = dot(ucur);
         issue(wg, next2, gcur);
+        issue(wu, next2, ucur);
         if (lane == 0 && valid) {
             s_g[row] = g;
-            s_on[row] = 0;
-            s_h[row] = 0.f;
+            const bool on = g > 0.f && u > 0.f;
+            s_on[row] = on ? 1 : 0;
+            s_h[row] = on ? g * u : 0.f;
         }
-        if (prev_row >= 0) {
-            const float u = dot(uprev);
-            if (lane == 0 && u > 0.f) {
-                s_on[prev_row] = 1;
-                s_h[prev_row] = s_g[prev_row] * u;
-            }
-        }
-        prev_row = open ? row : -1;
     }
 };
 
@@ -669,24 +666,18 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
     const WT *wd = reinterpret_cast<const WT *>(a.wd);
     GivenWave<WT, NC> gw{wg, wu, xt, s_row, H, nch, lane, xr, s_g, s_h, s_on};
 
-    // this wave's entries: wave, wave + 8, ...; first two gate rows in flight
+    // this wave's entries: wave, wave + 8, ...; two entries' gate and up rows in flight
     const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
     u32x4 g0[NC], g1[NC], u0[NC], u1[NC];
     gw.issue(wg, nrow > 0 ? wave : -1, g0);
+    gw.issue(wu, nrow > 0 ? wave : -1, u0);
     gw.issue(wg, nrow > 1 ? wave + kWaves : -1, g1);
-    int prev = -1;
+    gw.issue(wu, nrow > 1 ? wave + kWaves : -1, u1);
 #pragma unroll
     for (int i = 0; i < MR; i += 2) {
         const int r = wave + kWaves * i;
-        gw.step(r, i < nrow, i + 2 < nrow ? r + 2 * kWaves : -1, g0, u0, u1, prev);
-        gw.step(r + kWaves, i + 1 < nrow, i + 3 < nrow ? r + 3 * kWaves : -1, g1, u1, u0, prev);
-    }
-    if (prev >= 0) {
-        const float u = gw.dot(u1);
-        if (lane == 0 && u > 0.f) {
-            s_on[prev] = 1;
-            s_h[prev] = s_g[prev] * u;
-        }
+        gw.step(r, i < nrow, i + 2 < nrow ? r + 2 * kWaves : -1, g0, u0);
+        gw.step(r + kWaves, i + 1 < nrow, i + 3 < nrow ? r + 3 * kWaves : -1, g1, u1);
     }
     __syncthreads();
 

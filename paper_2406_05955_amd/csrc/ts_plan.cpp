@@ -208,8 +208,8 @@ bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtyp
 }
 
 // Chunk of list entries per workgroup: enough workgroups for one per compute
-// unit over the whole batch, a multiple of 8 (rows per wave x 8 waves), at
-// most 128; the ffn_tile knob overrides.
+// unit over the whole batch (one 8-wave workgroup fills a compute unit), a
+// multiple of 4, at most 128; the ffn_tile knob overrides.
 bool plan_given(int batch, int hidden, int inter, int max_count, ts_dtype dt, GivenPlan *p) {
     if (check_dims(batch, hidden, inter, dt) != TS_OK || max_count < 1 || max_count > kMaxGivenList) return false;
     GivenPlan q;
@@ -224,8 +224,8 @@ bool plan_given(int batch, int hidden, int inter, int max_count, ts_dtype dt, Gi
     int t = tuned_tile();
     if (t <= 0) {
         long long per = ((long long)max_count * batch + kTargetTiles - 1) / kTargetTiles;
-        per = (per + 7) / 8 * 8;
-        t = (int)std::max(8LL, std::min((long long)kMaxPipeTile, per));
+        per = (per + 3) / 4 * 4;
+        t = (int)std::max(4LL, std::min((long long)kMaxPipeTile, per));
     }
     q.chunk = std::min(t, kMaxPipeTile);
     q.nchunks = (max_count + q.chunk - 1) / q.chunk;
