@@ -17,7 +17,7 @@ per-launch HIP events, and the fp64 oracle
 timed on the host cores as a CPU baseline.
 
 Other workloads (--workload): sweep (gate bias for 50/75/90/95/99% sparsity),
-moe (Mixtral-shaped top-2 MoE layer, batch 1 and 16), batch (batch 8 and 32),
+moe (Mixtral-shaped top-2 MoE layer, batch 1, 16, 32, 64), batch (batch 8 and 32),
 given (predictor mode: each layer called with its exact gate set as the
 neuron list).
 """
@@ -355,7 +355,7 @@ def run_given_workload(args, ts, synth, torch):
 
 def batch_kernels(ts, torch, fn, steps):
     res = {}
-    for k in ("batch_dispatch", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
+    for k in ("moe_router", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
         n, ms = kernel_avg_ms(ts, torch, fn, steps, k)
         if n:
             res[k + "_us"] = ms * 1e3
@@ -465,13 +465,13 @@ class MoEStack:
 def run_moe_workload(args, ts, synth, torch):
     """Mixtral-shaped MoE layer: 8 experts (hidden 4096, inter 14336, bf16),
     top-2 softmax router, gate bias for 97% zero Combined activations inside
-    each expert (also the paper's 85% point), batch 1 and 16; 8 layers so a
-    step streams several GB."""
+    each expert (also the paper's 85% point at batch 1), batch 1, 16, 32 and
+    64; 8 layers so a step streams several GB."""
     out = []
     H, I, E, K, L = H_MISTRAL, I_MISTRAL, 8, 2, 8
-    for B in (1, 16):
+    for B in (1, 16, 32, 64):
         for sp_target, bias in ((0.97, -1.5548), (0.85, -0.5244)):
-            if B == 16 and sp_target == 0.85:
+            if B > 1 and sp_target == 0.85:
                 continue
             stack = MoEStack(ts, synth, L, B, H, I, E, K, gate_bias=bias, seed=4)
             sp, dn = stack.touched()

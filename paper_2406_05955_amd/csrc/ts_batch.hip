@@ -11,12 +11,12 @@
 //
 // A group is one weight set and the tokens routed to it: the FFN has one
 // group, the MoE layer one per expert (tokens listed on the device by
-// bx_dispatch, ascending).  x and Combined enter the matrix cores as two bf16
+// bx_prep, ascending).  x and Combined enter the matrix cores as two bf16
 // parts (v = hi + lo to 16 significant bits), so the products keep fp32-level
 // accuracy; with at most 8 token slots both parts share one 16-column MFMA
 // tile (columns 0-7 high, 8-15 low) and are added at the end.  Kernels:
-//   bx_dispatch  routing table -> per-group token lists and slots
-//   bx_prep      x of each group's tokens split into bf16 high and low parts
+//   bx_prep      routing table -> per-group token lists (MoE), and x of each
+//                group's tokens split into bf16 high and low parts
 //   bx_gate_up   per 32-neuron tile, 4 waves each a quarter of the hidden
 //                dimension with its own pipelined loads (no barrier inside
 //                the K loop): gate for all tokens, union of open gates, up
@@ -85,7 +85,6 @@ struct BxArgs {
     const int32_t *topk;     // [B][K] routed experts, or null (FFN)
     const float *topw;       // [B][K] routing weights, or null
     int32_t *gcount;         // [G]
-    int32_t *gtok;           // [G][bpad] token of each slot, -1 past the count
     int32_t *tslot;          // [B][K][2] (group, slot) of each routed token
     uint16_t *xhl;           // x fragments [G][hpad / 32][NX][64 lanes][8] bf16 (MFMA operand order)
     int32_t *cnt;            // [G][ntiles][2] |union G|, |union A|
@@ -100,73 +99,64 @@ struct BxArgs {
 };
 
 // ---------------------------------------------------------------------------
-// Routing table -> groups.  One wave; (token, rank) pairs are taken in
-// token-major order, so each expert's token list comes out ascending.
-__global__ __launch_bounds__(64) void bx_dispatch(BxArgs a) {
-    __shared__ int s_base[kMaxExperts];
-    const int lane = threadIdx.x;
-    if (!a.topk) {
-        for (int s = lane; s < a.bpad; s += 64) a.gtok[s] = s < a.B ? s : -1;
-        for (int t = lane; t < a.B; t += 64) {
-            a.tslot[t * 2] = 0;
-            a.tslot[t * 2 + 1] = t;
-        }
-        if (lane == 0) a.gcount[0] = a.B;
-        return;
-    }
-    for (int e = lane; e < a.G; e += 64) s_base[e] = 0;
-    for (int i = lane; i < a.G * a.bpad; i += 64) a.gtok[i] = -1;
-    __syncthreads();
-    const int np = a.B * a.K;
-    for (int p0 = 0; p0 < np; p0 += 64) {
-        const int p = p0 + lane;
-        const int e = p < np ? a.topk[p] : -1;
-        for (int ex = 0; ex < a.G; ++ex) {
-            const uint64_t m = __ballot(e == ex);
-            if (m == 0) continue;
-            const int base = s_base[ex];
-            if (e == ex) {
-                const int rank = base + lane_prefix(m, lane);
-                a.gtok[ex * a.bpad + rank] = p / a.K;
-                a.tslot[p * 2] = ex;
-                a.tslot[p * 2 + 1] = rank;
-            }
-            __syncthreads();  // one wave: orders the read of s_base before the update
-            if (lane == 0) s_base[ex] = base + __popcll(m);
-            __syncthreads();
-        }
-    }
-    for (int e = lane; e < a.G; e += 64) a.gcount[e] = s_base[e];
-}
-
 // x of each group's token slots as MFMA operand fragments: for k-step ks (32
 // wide) and fragment f, lane (lm, lq) holds the 8 values at k = 32 ks + 8 lq
 // of column lm, column = (high or low part, token slot); fragments are 1 KB
 // contiguous, so a wave loads one with a single fully coalesced instruction.
 // Zero past the token count and past H (to hpad).  One thread per (group,
-// k-step, fragment, lane).  Without a routing table (the FFN) the slots are
-// the tokens themselves and block 0 also writes the group table.
+// k-step, fragment, lane); a block's 256 threads belong to one group (hpad /
+// 32 k-steps per group is a multiple of 32).  Without a routing table (the
+// FFN) the slots are the tokens themselves.  With one (the MoE layer), one
+// wave of each block lists its group's tokens: the (token, rank) pairs are
+// scanned in token-major order, so each expert's list comes out ascending.
+// The group's first block also writes the group tables (token count, and
+// the (group, slot) of each routed pair for the reduce and the report).
 template <int TOK>
 __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
     using S = Bx<TOK>;
     constexpr int NX = S::NX;
-    if (!a.topk && blockIdx.x == 0) {
+    __shared__ int s_tok[TOK];
+    const int nks = a.hpad / 32;
+    const int g = (blockIdx.x * 4) / (NX * nks);
+    const bool first = blockIdx.x * 4 == g * NX * nks;
+    if (a.topk) {
+        if (threadIdx.x < 64) {
+            const int lane = threadIdx.x;
+            const int np = a.B * a.K;
+            int base = 0;
+            for (int p0 = 0; p0 < np; p0 += 64) {
+                const int p = p0 + lane;
+                const bool mine = p < np && a.topk[p] == g;
+                const uint64_t m = __ballot(mine);
+                if (mine) {
+                    const int rank = base + lane_prefix(m, lane);  // < TOK: top-k experts are distinct
+                    s_tok[rank] = p / a.K;
+                    if (first) {
+                        a.tslot[p * 2] = g;
+                        a.tslot[p * 2 + 1] = rank;
+                    }
+                }
+                base += __popcll(m);
+            }
+            for (int sl = base + lane; sl < TOK; sl += 64) s_tok[sl] = -1;
+            if (first && lane == 0) a.gcount[g] = base;
+        }
+        __syncthreads();
+    } else if (blockIdx.x == 0) {
         for (int t = threadIdx.x; t < a.B; t += 256) {
             a.tslot[t * 2] = 0;
             a.tslot[t * 2 + 1] = t;
         }
         if (threadIdx.x == 0) a.gcount[0] = a.B;
     }
-    const int nks = a.hpad / 32;
     const int idx = blockIdx.x * 256 + threadIdx.x;
     if (idx >= a.G * nks * NX * 64) return;
     const int lane = idx & 63, lm = lane & 15, lq = lane >> 4;
     const int f = (idx >> 6) % NX;
     const int ks = (idx >> 6) / NX % nks;
-    const int g = (idx >> 6) / NX / nks;
     const int hl = S::PACK ? (lm >> 3) : (f & 1);
     const int slot = S::PACK ? (lm & 7) : 16 * (f >> 1) + lm;
-    const int t = a.topk ? a.gtok[g * TOK + slot] : (slot < a.B ? slot : -1);
+    const int t = a.topk ? s_tok[slot] : (slot < a.B ? slot : -1);
     const int k0 = ks * 32 + 8 * lq;
     float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (t >= 0 && k0 < a.H) {  // H is a multiple of 8, so all 8 are in range
@@ -915,7 +905,6 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     a.topk = topk;
     a.topw = topw;
     a.gcount = ws_at<int32_t>(ws, p.off_gcount);
-    a.gtok = ws_at<int32_t>(ws, p.off_gtok);
     a.tslot = ws_at<int32_t>(ws, p.off_tslot);
     a.xhl = ws_at<uint16_t>(ws, p.off_xhl);
     a.cnt = ws_at<int32_t>(ws, p.off_cnt);
@@ -928,7 +917,6 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     const bool want_lists = stats && (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx);
     a.want_masks = want_lists ? 1 : 0;
 
-    if (topk) launch("batch_dispatch", bx_dispatch, dim3(1), dim3(64), st, a);
     switch (p.tok) {
     case 8: launch_tok<8>(p, a, st); break;
     case 16: launch_tok<16>(p, a, st); break;

@@ -182,8 +182,6 @@ bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtyp
     size_t off = 0;
     q.off_gcount = off;  // tokens per group
     off = align256(off + G * sizeof(int32_t));
-    q.off_gtok = off;    // token of each (group, slot)
-    off = align256(off + G * q.tok * sizeof(int32_t));
     q.off_tslot = off;   // (group, slot) of each (token, routed rank)
     off = align256(off + (size_t)batch * top_k * 2 * sizeof(int32_t));
     q.off_xhl = off;     // x split into bf16 high and low parts: [G][2][tok][hpad]

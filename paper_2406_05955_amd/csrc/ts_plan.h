@@ -73,7 +73,7 @@ struct BatchPlan {
     int nslices = 0;     // 128-column slices of the down kernel
     int nchunks = 0;     // tile chunks per group in the down kernel
     int tpc = 0;         // tiles per chunk (<= kBxChunkTiles)
-    size_t off_gcount = 0, off_gtok = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_arow = 0, off_hfrag = 0;
+    size_t off_gcount = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_arow = 0, off_hfrag = 0;
     size_t off_gmask = 0, off_amask = 0, off_partial = 0, off_union = 0;
     size_t total = 0;
 };

@@ -130,8 +130,9 @@ def test_moe_batch_shapes(B, H, I, E, K):
     moe_check(m)
 
 
-def test_moe_batch_mixtral_shape():
-    L = synth.make_moe_stack_torch(1, 16, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=3,
+@pytest.mark.parametrize("B", [16, 32])
+def test_moe_batch_mixtral_shape(B):
+    L = synth.make_moe_stack_torch(1, B, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=3,
                                    device=DEV)
     h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
     m = synth.MoEInputs(x=L["x"][0].cpu().numpy(), w_router=h(L["w_router"][0]), w_gate=h(L["w_gate"][0]),
