@@ -49,6 +49,8 @@ def _bind(lib):
     lib.or_moe.restype = ctypes.c_int
     lib.or_ffn_given.argtypes = [vp, vp, vp, vp, ip, ip, ip, ip, vp, vp, ip, dp, vp, vp, ip]
     lib.or_ffn_given.restype = ctypes.c_int
+    lib.or_ffn_act.argtypes = [vp, vp, vp, vp, ip, ip, ip, ip, ip, ctypes.c_double, dp, dp, dp, ip]
+    lib.or_ffn_act.restype = ctypes.c_int
     lib.or_max_threads.argtypes = []
     lib.or_max_threads.restype = ctypes.c_int
     return lib
@@ -127,6 +129,52 @@ def ffn(x, w_gate, w_up, w_down_t, dtype: int, threads: int = 0, lib=None) -> FF
     if rc != 0:
         raise RuntimeError("or_ffn failed")
     return FFNResult(y=y, g=g, u=u)
+
+
+ACT_DRELU = 0
+ACT_RELU_GATE = 1
+
+
+@dataclass
+class ActResult:
+    y: np.ndarray       # fp64 [B][H]
+    g: np.ndarray       # fp64 [B][I] gate projection before the activation
+    u: np.ndarray       # fp64 [B][I] up projection
+    act: int
+    tau: float
+
+    def gate_set(self, t: int) -> np.ndarray:
+        """Neurons whose gate passes the activation's threshold (ascending)."""
+        return np.nonzero(self.g[t] > self.tau)[0].astype(np.int32)
+
+    def active_set(self, t: int) -> np.ndarray:
+        """Neurons with a non-zero Combined activation (ascending)."""
+        if self.act == ACT_DRELU:
+            m = (self.g[t] > 0.0) & (self.u[t] > 0.0)
+        else:
+            m = (self.g[t] > self.tau) & (self.u[t] != 0.0)
+        return np.nonzero(m)[0].astype(np.int32)
+
+
+def ffn_act(x, w_gate, w_up, w_down_t, dtype: int, act: int, tau: float = 0.0, threads: int = 0,
+            lib=None) -> ActResult:
+    """FFN in fp64 with act 0 = dReLU (tau 0) or act 1 = gate-only ReLU with
+    threshold tau: Combined = max(0, g - tau) * u (ReGLU at tau = 0)."""
+    lib = lib or _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    B, H = x.shape
+    wg, wu, wd = (_weights(w, dtype) for w in (w_gate, w_up, w_down_t))
+    I = wg.shape[0]
+    y = np.empty((B, H), np.float64)
+    g = np.empty((B, I), np.float64)
+    u = np.empty((B, I), np.float64)
+    rc = lib.or_ffn_act(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), dtype, B, H, I, int(act), float(tau), _ptr(y),
+                        _ptr(g), _ptr(u), int(threads))
+    if rc != 0:
+        raise RuntimeError("or_ffn_act failed")
+    return ActResult(y=y, g=g, u=u, act=int(act), tau=float(tau))
 
 
 @dataclass

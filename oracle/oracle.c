@@ -135,6 +135,67 @@ int or_ffn(const float *x, const void *wg, const void *wu, const void *wdt, int 
 }
 
 /*
+ * The FFN with a gate-only ReLU (section 2, Eq. gated-MLP with F_act = ReLU,
+ * i.e. ReGLU, the ReLUfication baseline of section 3.1) or its shifted form
+ * (section 3.1: shifted-ReLU moves the ReLU threshold of the gate to mask
+ * more of it; read here as max(0, gate - tau)), next to dReLU:
+ *   act 0 (dReLU):  Combined_i = max(0, g_i) * max(0, u_i)      (tau must be 0)
+ *   act 1 (ReGLU):  Combined_i = max(0, g_i - tau) * u_i          (up unmasked)
+ * Same layout, order and outputs as or_ffn (g_out / u_out: the projections
+ * before any activation).  Returns 0, or -1 on bad arguments.
+ */
+int or_ffn_act(const float *x, const void *wg, const void *wu, const void *wdt, int dtype, int B, int H,
+               int I, int act, double tau, double *y, double *g_out, double *u_out, int nthreads)
+{
+    if (!x || !wg || !wu || !wdt || !y || B < 0 || H <= 0 || I < 0 || (dtype != OR_F32 && dtype != OR_BF16) ||
+        (act != 0 && act != 1) || (act == 0 && tau != 0.0) || !isfinite(tau))
+        return -1;
+    nthreads = set_threads(nthreads);
+    size_t nI = I > 0 ? (size_t)I : 1;
+    double *ha = malloc(nI * sizeof *ha);
+    if (!ha)
+        return -1;
+    for (int t = 0; t < B; ++t) {
+        const float *xt = x + (size_t)t * H;
+        int i;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+        for (i = 0; i < I; ++i) {
+            double sg = 0.0, su = 0.0;
+            size_t row = (size_t)i * (size_t)H;
+            for (int j = 0; j < H; ++j) {
+                sg += load_w(wg, dtype, row + j) * (double)xt[j];
+                su += load_w(wu, dtype, row + j) * (double)xt[j];
+            }
+            if (g_out)
+                g_out[(size_t)t * I + i] = sg;
+            if (u_out)
+                u_out[(size_t)t * I + i] = su;
+            if (act == 0)
+                ha[i] = (sg > 0.0 && su > 0.0) ? sg * su : 0.0;
+            else
+                ha[i] = sg > tau ? (sg - tau) * su : 0.0;
+        }
+        double *yt = y + (size_t)t * H;
+        int nblk = (H + 63) / 64;
+        int b;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+        for (b = 0; b < nblk; ++b) {
+            int j0 = b * 64, j1 = j0 + 64 < H ? j0 + 64 : H;
+            for (int j = j0; j < j1; ++j)
+                yt[j] = 0.0;
+            for (int ii = 0; ii < I; ++ii) {
+                double hv = ha[ii];
+                size_t row = (size_t)ii * (size_t)H;
+                for (int j = j0; j < j1; ++j)
+                    yt[j] += load_w(wdt, dtype, row + j) * hv;
+            }
+        }
+    }
+    free(ha);
+    return 0;
+}
+
+/*
  * The dReLU FFN evaluated over given neuron lists: the interface an
  * activation predictor drives (section 7 of the paper: the inference engine
  * evaluates only the neurons predicted active).  For token t only the

@@ -372,6 +372,81 @@ def pin_given_exact_sets_bitwise(lib=None):
         assert not np.allclose(r.y[0], rd.y[0], rtol=1e-9, atol=0)
 
 
+# ----------------------------------------------------------------------------
+# Gate-only ReLU (ReGLU) and its shifted form
+
+
+def pin_act_bruteforce(lib=None):
+    """Exact rational evaluation of max(0, g - tau) * u summed over neurons,
+    tau in {0, 1/4}, within the fp64 forward-error bound."""
+    for dtype in (synth.F32, synth.BF16):
+        for k, (B, H, I) in enumerate([(1, 4, 6), (2, 8, 16), (1, 5, 9)]):
+            inp = synth.make_ffn(B, H, I, gate_bias=0.1, dtype=dtype, seed=[51, k, dtype])
+            wg, wu, wd = (_as_fractions(w, dtype) for w in (inp.w_gate, inp.w_up, inp.w_down_t))
+            for tau in (0.0, 0.25):
+                r = oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, oracle.ACT_RELU_GATE, tau,
+                                   threads=1, lib=lib)
+                ft = Fraction(tau)
+                for t in range(B):
+                    x = [Fraction(float(v)) for v in inp.x[t]]
+                    g = [sum((wg[i][j] * x[j] for j in range(H)), Fraction(0)) for i in range(I)]
+                    u = [sum((wu[i][j] * x[j] for j in range(H)), Fraction(0)) for i in range(I)]
+                    h = [(g[i] - ft) * u[i] if g[i] > ft else Fraction(0) for i in range(I)]
+                    eh = []
+                    for i in range(I):
+                        eg = gamma(H) * float(sum(abs(wg[i][j] * x[j]) for j in range(H)))
+                        eu = gamma(H) * float(sum(abs(wu[i][j] * x[j]) for j in range(H)))
+                        ad, au = abs(float(g[i] - ft)), abs(float(u[i]))
+                        eh.append((ad + eg) * eu + au * eg + 2 * U * (ad + eg) * (au + eu))
+                    for j in range(H):
+                        y = sum((wd[i][j] * h[i] for i in range(I)), Fraction(0))
+                        s_abs = sum(abs(float(wd[i][j])) * (abs(float(h[i])) + eh[i]) for i in range(I))
+                        bound = gamma(I) * s_abs + sum(abs(float(wd[i][j])) * eh[i] for i in range(I))
+                        assert _within(r.y[t, j], y, bound), (dtype, B, H, I, tau, t, j)
+
+
+def pin_act_numpy(lib=None):
+    """ReGLU / shifted gate against numpy fp64; the gate-only ReLU leaves the
+    up branch unmasked, so the active set is the gate set (A = G)."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 200, 500, gate_bias=-0.84, dtype=dtype, seed=52)
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        x = inp.x.astype(np.float64)
+        g = x @ up(inp.w_gate).astype(np.float64).T
+        u = x @ up(inp.w_up).astype(np.float64).T
+        wd = up(inp.w_down_t).astype(np.float64)
+        for tau in (0.0, 0.3):
+            r = oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, oracle.ACT_RELU_GATE, tau, lib=lib)
+            h = np.where(g > tau, (g - tau) * u, 0.0)
+            y = h @ wd
+            assert np.allclose(r.y, y, rtol=1e-12, atol=1e-12 * np.abs(y).max())
+            for t in range(2):
+                ok = np.abs(g[t] - tau) > 1e-9
+                assert np.array_equal((r.g[t] > tau)[ok], (g[t] > tau)[ok])
+                assert np.array_equal(r.active_set(t), r.gate_set(t))
+        r = oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, oracle.ACT_RELU_GATE, 1e6, lib=lib)
+        assert np.all(r.y == 0.0)
+
+
+def pin_act_drelu_is_dense_oracle(lib=None):
+    """act 0 is the dReLU of or_ffn, bit for bit; a non-zero tau is rejected
+    for it."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 96, 300, gate_bias=-0.84, dtype=dtype, seed=53)
+        ra = oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, oracle.ACT_DRELU, 0.0, lib=lib)
+        rd = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, lib=lib)
+        assert np.array_equal(ra.y.view(np.uint64), rd.y.view(np.uint64))
+        for t in range(2):
+            assert np.array_equal(ra.active_set(t), rd.active_set(t))
+    try:
+        oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, oracle.ACT_DRELU, 0.5, lib=lib)
+    except RuntimeError:
+        pass
+    else:
+        raise AssertionError("dReLU with a threshold accepted")
+
+
 ALL_PINS = [pin_ffn_handworked, pin_moe_handworked, pin_ffn_bruteforce, pin_moe_bruteforce,
             pin_ffn_zero_bias, pin_ffn_all_active_numpy, pin_ffn_sets_numpy, pin_ffn_skipzero_bitwise,
-            pin_moe_special_cases, pin_given_bruteforce, pin_given_numpy, pin_given_exact_sets_bitwise]
+            pin_moe_special_cases, pin_given_bruteforce, pin_given_numpy, pin_given_exact_sets_bitwise,
+            pin_act_bruteforce, pin_act_numpy, pin_act_drelu_is_dense_oracle]

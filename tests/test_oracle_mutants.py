@@ -28,6 +28,10 @@ MUTANTS = {
     "moe_wrong_expert_down": ("const char *base_d = (const char *)wdt + (size_t)e * expert_bytes;",
                               "const char *base_d = (const char *)wdt;"),
     "moe_rank_weight_swap": ("yt[j] += w[rank] * ye[j];", "yt[j] += w[K - 1 - rank] * ye[j];"),
+    "act_shift_sign": ("ha[i] = sg > tau ? (sg - tau) * su : 0.0;", "ha[i] = sg > tau ? (sg + tau) * su : 0.0;"),
+    "act_unshifted_product": ("ha[i] = sg > tau ? (sg - tau) * su : 0.0;", "ha[i] = sg > tau ? sg * su : 0.0;"),
+    "act_up_masked": ("ha[i] = sg > tau ? (sg - tau) * su : 0.0;",
+                      "ha[i] = (sg > tau && su > 0.0) ? (sg - tau) * su : 0.0;"),
     "given_gate_only_relu": ("hl[k] = (sg > 0.0 && su > 0.0) ? sg * su : 0.0;", "hl[k] = (sg > 0.0) ? sg * su : 0.0;"),
     "given_count_ignored": ("int n = count[t] < 0 ? 0 : (count[t] > maxc ? maxc : count[t]);", "int n = maxc;"),
     "given_down_list_position": ("double hv = hl[kk];\n                size_t row = (size_t)i * (size_t)H;",
