@@ -112,6 +112,31 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
                         ts_dtype wdtype, int batch, int hidden, int inter, float *out,
                         const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
 
+/* Activation of the FFN (ts_ffn_sparse_act). */
+typedef enum {
+    TS_ACT_DRELU = 0,     /* Eq. drelu: Combined = max(0, gate) * max(0, up) */
+    TS_ACT_RELU_GATE = 1  /* gate-only ReLU with threshold tau: Combined = max(0, gate - tau) * up */
+} ts_act;
+
+/*
+ * The sparse FFN with a choice of activation, to set dReLU beside the
+ * ReLUfication baselines of section 3.1: TS_ACT_RELU_GATE with tau = 0 is
+ * ReGLU (Eq. gated-MLP with F_act = ReLU, section 2), tau > 0 its shifted
+ * form (section 3.1: the threshold of the gate's ReLU moved to mask more of
+ * it; read as max(0, gate - tau)).  The up branch is not masked, so a neuron
+ * whose gate passes the threshold is active unless its up projection is
+ * exactly zero (A = G): W_gate is read whole, and the W_up and W_down_t rows
+ * of G.  TS_ACT_DRELU requires tau == 0 and is ts_ffn_sparse.
+ * The activity report gives G_t = {gate > tau} and A_t = {Combined != 0}.
+ * Other arguments as ts_ffn_sparse, same workspace size.  TS_ACT_RELU_GATE
+ * runs the single-token kernels per token (the batched matrix-core path
+ * serves dReLU only).  An unknown `act`, a non-finite tau, or a non-zero tau
+ * with TS_ACT_DRELU returns TS_ERR_SHAPE.
+ */
+ts_status ts_ffn_sparse_act(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                            ts_dtype wdtype, int batch, int hidden, int inter, ts_act act, float tau,
+                            float *out, const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
 /*
  * Dense comparator: the same function (Eq. gated-MLP with dReLU) computed
  * over every neuron, reading all three matrices in full.  Same arguments as

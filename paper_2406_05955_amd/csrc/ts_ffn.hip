@@ -31,6 +31,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 
 #include "ts_batch.h"
@@ -113,7 +114,19 @@ struct SlotArgs {
     int E, K;
     int32_t *ridx;
     float *rw;
+    // Activation: 0 = dReLU (Eq. drelu), 1 = gate-only ReLU with threshold
+    // `tau` (Combined = max(0, gate - tau) * up: ReGLU at tau = 0).
+    int act;
+    float tau;
 };
+
+// The open-gate threshold and the Combined activation of a neuron whose
+// gate passed it, for either activation.
+__device__ __forceinline__ float gate_threshold(int act, float tau) { return act ? tau : 0.f; }
+__device__ __forceinline__ bool combined_nonzero(int act, float u) { return act ? u != 0.f : u > 0.f; }
+__device__ __forceinline__ float combined_value(int act, float tau, float g, float u) {
+    return act ? (g - tau) * u : g * u;
+}
 
 // Softmax over the E logits, the top K (strictly larger wins, so the lower
 // index wins exact ties) and their renormalised weights.  One thread.
@@ -196,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
     // ---- ballot compaction of the open gates --------------------------------
     if (wave == 0) {
         const bool in = lane < nt;
-        const bool p = in && (DENSE || s_g[lane] > 0.f);
+        const bool p = in && (DENSE || s_g[lane] > gate_threshold(a.act, a.tau));
         const uint64_t m = __ballot(p);
         if (p) s_gl[lane_prefix(m, lane)] = lane;
         if (lane == 0) s_n[0] = __popcll(m);
@@ -222,9 +235,9 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
             for (int k = 0; k < RIF; ++k) {
                 if (valid[k]) {
                     const float g = s_g[li[k]];
-                    const bool on = g > 0.f && u[k] > 0.f;
+                    const bool on = g > gate_threshold(a.act, a.tau) && combined_nonzero(a.act, u[k]);
                     s_on[q + k * kWaves] = on;
-                    s_h[q + k * kWaves] = on ? g * u[k] : 0.f;
+                    s_h[q + k * kWaves] = on ? combined_value(a.act, a.tau, g, u[k]) : 0.f;
                 }
             }
         }
@@ -319,6 +332,8 @@ struct PipeWave {
     static constexpr int CE = WTraits<WT>::CE;
     __amdgpu_buffer_rsrc_t rg, ru;  // the tile's W_gate / W_up rows
     int H, nch, lane;
+    int act;
+    float tau;
     float (&xr)[NC][CE];
     float *s_g, *s_h;
     int *s_on;
@@ -354,7 +369,7 @@ struct PipeWave {
     __device__ void step(int row, bool valid, int next2, u32x4 (&gcur)[NC], u32x4 (&ucur)[NC],
                          u32x4 (&uprev)[NC], int &prev_row) {
         const float g = dot(gcur);
-        const bool open = valid && g > 0.f;
+        const bool open = valid && g > gate_threshold(act, tau);
         issue(ru, open ? row : -1, ucur);
         issue(rg, next2, gcur);
         if (lane == 0 && valid) {
@@ -362,14 +377,15 @@ struct PipeWave {
             s_on[row] = 0;
             s_h[row] = 0.f;
         }
-        if (prev_row >= 0) {
-            const float u = dot(uprev);
-            if (lane == 0 && u > 0.f) {
-                s_on[prev_row] = 1;
-                s_h[prev_row] = s_g[prev_row] * u;
-            }
-        }
+        if (prev_row >= 0) finish_up(prev_row, dot(uprev));
         prev_row = open ? row : -1;
+    }
+    // Up dot of an open row done: its Combined activation.
+    __device__ void finish_up(int row, float u) {
+        if (lane == 0 && combined_nonzero(act, u)) {
+            s_on[row] = 1;
+            s_h[row] = combined_value(act, tau, s_g[row], u);
+        }
     }
 };
 
@@ -449,7 +465,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff + (size_t)n0 * H;
     // buffer resources over the tile's rows (at most 128 rows of 32 KB)
     const uint32_t tbytes = (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT);
-    PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H, nch, lane, xr, s_g, s_h, s_on};
+    PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H, nch, lane, a.act, a.tau, xr, s_g, s_h, s_on};
 
     // this wave's rows: wave, wave + 8, ...; first two gate rows in flight
     const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
@@ -466,13 +482,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
         pw.step(r, i < nrow, i + 2 < nrow ? r + 2 * kWaves : -1, g0, u0, u1, prev);
         pw.step(r + kWaves, i + 1 < nrow, i + 3 < nrow ? r + 3 * kWaves : -1, g1, u1, u0, prev);
     }
-    if (prev >= 0) {  // the last step's up loads sit in u1
-        const float u = pw.dot(u1);
-        if (lane == 0 && u > 0.f) {
-            s_on[prev] = 1;
-            s_h[prev] = s_g[prev] * u;
-        }
-    }
+    if (prev >= 0) pw.finish_up(prev, pw.dot(u1));  // the last step's up loads sit in u1
     __syncthreads();
 
     // ---- ballots: open gates (report) and non-zero Combined activations ------
@@ -481,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
         for (int h = 0; h < kMaxPipeTile / 64; ++h) {
             const int r = lane + 64 * h;
             const bool in = r < nt;
-            const bool pg = in && s_g[r] > 0.f;
+            const bool pg = in && s_g[r] > gate_threshold(a.act, a.tau);
             const uint64_t mg = __ballot(pg);
             if (pg && a.want_seg) a.gseg[pr * a.tile + ng + lane_prefix(mg, lane)] = n0 + r;
             const bool pa = in && s_on[r];
@@ -1387,9 +1397,11 @@ struct RouterFold {
 ts_status run_fused(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
                     size_t expert_stride, ts_dtype dt, bool dense, const SlotPlan &p, float *out,
                     const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool pipe,
-                    const RouterFold *rf = nullptr) {
+                    const RouterFold *rf = nullptr, int act = 0, float tau = 0.f) {
     const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
     SlotArgs a;
+    a.act = act;
+    a.tau = tau;
     a.wr = rf ? rf->wr : nullptr;
     a.E = rf ? rf->E : 0;
     a.K = rf ? rf->K : 0;
@@ -1559,6 +1571,23 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
         return TS_OK;
     }
     return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, false, p, out, nullptr, stats, ws, st);
+}
+
+ts_status ts_ffn_sparse_act(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                            ts_dtype wdtype, int batch, int hidden, int inter, ts_act act, float tau, float *out,
+                            const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream) {
+    if ((act != TS_ACT_DRELU && act != TS_ACT_RELU_GATE) || !std::isfinite(tau) ||
+        (act == TS_ACT_DRELU && tau != 0.f))
+        return TS_ERR_SHAPE;
+    if (act == TS_ACT_DRELU)
+        return ts_ffn_sparse(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws, ws_bytes,
+                             stream);
+    ts::SlotPlan p;
+    ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws,
+                                     ws_bytes, &p);
+    if (s != TS_OK) return s;
+    return ts::run_fused(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, false, p, out, nullptr, stats, ws,
+                         static_cast<hipStream_t>(stream), true, nullptr, 1, tau);
 }
 
 ts_status ts_ffn_dense(const float *x, const void *w_gate, const void *w_up, const void *w_down_t, ts_dtype wdtype,

@@ -148,3 +148,21 @@ def test_given_checks():
     assert call(stats=ctypes.byref(st)) == UNSUP
     st = ts.ffn_stats_t(A + 2, None, None, None, None)
     assert call(stats=ctypes.byref(st)) == ALIGN
+
+
+def test_act_checks():
+    f = ts.lib.ts_ffn_sparse_act
+
+    def call(act=1, tau=0.0, B=1, H=4096, I=14336, out=A, ws=A, wsb=1 << 40, x=A):
+        return f(x, A, A, A, 1, B, H, I, act, tau, out, None, ws, wsb, None)
+    assert call(act=2) == SHAPE
+    assert call(act=-1) == SHAPE
+    assert call(act=0, tau=0.5) == SHAPE
+    assert call(tau=float("nan")) == SHAPE
+    assert call(tau=float("inf")) == SHAPE
+    assert call(x=None) == NULL
+    assert call(out=A + 4) == ALIGN
+    need = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
+    assert call(wsb=need - 1) == WS
+    assert call(act=0, wsb=need - 1) == WS
+    assert call(B=0) == SHAPE

@@ -1,0 +1,82 @@
+"""Parity of the gate-only ReLU variants (ts_ffn_sparse_act: ReGLU and its
+shifted form) against the fp64 oracle's or_ffn_act, through the C ABI.
+
+Tolerances as for dReLU: relative L2 of the output <= 1e-5 with fp32 weights
+and <= 1e-2 with bf16 weights.  Sets: G = {gate > tau} and A = {Combined !=
+0} must match the oracle exactly on every neuron whose gate lies at least
+1e-6 (fp32) / 1e-4 (bf16) away from tau; with the up branch unmasked, A = G
+on these inputs (no up projection is exactly zero)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import compare_sets, ffn_inputs_to_dev, list_of, rel_l2
+from paper_2406_05955_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ts = pytest.importorskip("paper_2406_05955_amd.binding") if torch.cuda.is_available() else None
+
+
+def check(inp, tau):
+    B, H, I = inp.shape
+    ref = oracle.ffn_act(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype, oracle.ACT_RELU_GATE, tau)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    out, st = ts.ffn_sparse_act(x, wg, wu, wd, ts.TS_ACT_RELU_GATE, tau, stats=True)
+    torch.cuda.synchronize()
+    err = rel_l2(out.cpu().numpy(), ref.y)
+    assert err <= (1e-5 if inp.dtype == synth.F32 else 1e-2), (B, H, I, tau, err)
+    thr = 1e-6 if inp.dtype == synth.F32 else 1e-4
+    for t in range(B):
+        keep = np.abs(ref.g[t] - tau) >= thr
+        assert compare_sets(list_of(st, "gate_idx", t, "n_gate"), ref.g[t] > tau, keep) == 0
+        want_a = np.zeros(I, bool)
+        want_a[ref.active_set(t)] = True
+        assert compare_sets(list_of(st, "active_idx", t, "n_active"), want_a, keep) == 0
+        assert np.array_equal(ref.active_set(t), ref.gate_set(t))  # A = G
+        if keep.all():
+            assert int(st["n_gate"][t]) == int(st["n_active"][t]) == len(ref.gate_set(t))
+    return out, ref
+
+
+@pytest.mark.parametrize("B,H,I,dtype,tau", [
+    (1, 512, 1792, synth.F32, 0.0),     # the small fp32 workload's shape: ReGLU
+    (1, 512, 1792, synth.F32, 0.25),    # shifted
+    (3, 520, 999, synth.BF16, 0.1),     # ragged, several tokens (per-token kernels)
+    (2, 4096, 2048, synth.F32, 0.0),    # fp32 rows of 1024 chunks: the fused kernel
+    (4, 2048, 3000, synth.BF16, 0.3),
+])
+def test_act_shapes(B, H, I, dtype, tau):
+    inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[61, B, H, I])
+    check(inp, tau)
+
+
+def test_act_mistral_shape():
+    inp = synth.make_ffn(1, 4096, 14336, gate_bias=-0.8416, dtype=synth.BF16, seed=62)
+    out, ref = check(inp, 0.0)
+    assert rel_l2(out.cpu().numpy(), ref.y) <= 1e-4  # same bf16 values, fp32 accumulation
+
+
+def test_act_drelu_is_sparse():
+    """act = dReLU is ts_ffn_sparse, bit for bit."""
+    inp = synth.make_ffn(1, 1024, 2000, gate_bias=-0.84, dtype=synth.BF16, seed=63)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    a = ts.ffn_sparse_act(x, wg, wu, wd, ts.TS_ACT_DRELU, 0.0).clone()
+    b = ts.ffn_sparse(x, wg, wu, wd)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def test_act_reglu_differs_from_drelu_and_reads_more_rows():
+    """At equal gate sparsity ReGLU keeps the negative-up neurons: its active
+    set is G, about twice dReLU's A."""
+    inp = synth.make_ffn(1, 1024, 4000, gate_bias=-0.84, dtype=synth.BF16, seed=64)
+    x, wg, wu, wd = ffn_inputs_to_dev(inp)
+    _, sr = ts.ffn_sparse_act(x, wg, wu, wd, ts.TS_ACT_RELU_GATE, 0.0, stats=True)
+    _, sd = ts.ffn_sparse(x, wg, wu, wd, stats=True)
+    torch.cuda.synchronize()
+    assert int(sr["n_gate"][0]) == int(sd["n_gate"][0])
+    na_r, na_d = int(sr["n_active"][0]), int(sd["n_active"][0])
+    assert na_r == int(sr["n_gate"][0])
+    assert 1.6 * na_d < na_r < 2.4 * na_d
