@@ -19,7 +19,7 @@ timed on the host cores as a CPU baseline.
 Other workloads (--workload): sweep (gate bias for 50/75/90/95/99% sparsity),
 moe (Mixtral-shaped top-2 MoE layer, batch 1, 16, 32, 64), batch (batch 8 and 32),
 given (predictor mode: each layer called with its exact gate set as the
-neuron list).
+neuron list), act (dReLU beside ReGLU and the shifted gate-only ReLU).
 """
 from __future__ import annotations
 
@@ -47,7 +47,8 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=32)
-    ap.add_argument("--workload", default="mistral", choices=["mistral", "sweep", "moe", "batch", "given", "all"])
+    ap.add_argument("--workload", default="mistral",
+                    choices=["mistral", "sweep", "moe", "batch", "given", "act", "all"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle CPU-baseline leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -353,6 +354,47 @@ def run_given_workload(args, ts, synth, torch):
     return out
 
 
+def run_act_workload(args, ts, synth, torch):
+    """Activations side by side on the Mistral-shaped stack, batch 1
+    (ts_ffn_sparse_act): dReLU and ReGLU at the same gate bias (20% of the
+    gates open), and the shifted gate-only ReLU with its threshold set for
+    10% open gates (90% zero Combined activations, as dReLU's point)."""
+    out = []
+    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
+    b = -0.8416
+    stack = Stack(ts, synth, L, 1, H, I, gate_bias=b, seed=5)
+    d = stack.data
+    td = timed(torch, stack.step_dense, args.steps, args.warmup)
+    f = ts.lib.ts_ffn_sparse_act
+    # gate ~ N(b, ~1): P(gate > tau) = 0.1 at tau = b + 1.2816
+    for name, act, tau in (("drelu", ts.TS_ACT_DRELU, 0.0), ("reglu", ts.TS_ACT_RELU_GATE, 0.0),
+                           ("shifted_relu_gate", ts.TS_ACT_RELU_GATE, b + 1.2816)):
+        counts = []
+        for l in range(L):
+            _, st = ts.ffn_sparse_act(d["x"][l], d["w_gate"][l], d["w_up"][l], d["w_down_t"][l], act, tau,
+                                      stats=True)
+            torch.cuda.synchronize()
+            counts.append((int(st["n_gate"][0]), int(st["n_active"][0])))
+
+        def step():
+            for a in stack.args:
+                rc = f(*a[:8], act, ctypes.c_float(tau), a[8], None, stack.ws.data_ptr(), stack.wsb, stack.stream)
+                if rc:
+                    raise RuntimeError(f"ts_ffn_sparse_act -> {rc}")
+        t = timed(torch, step, args.steps, args.warmup)
+        alg = sum(2 * H * (I + ng + na) + 8 * H for ng, na in counts) / L
+        dense = 3 * 2 * H * I + 8 * H
+        out.append({"workload": "mistral7b_ffn_stack_bf16_b1_activation", "activation": name, "tau": tau,
+                    "gate_fraction": sum(c[0] for c in counts) / (L * I),
+                    "active_fraction": sum(c[1] for c in counts) / (L * I),
+                    "sparse_tokens_per_s_layer": L / t, "dense_tokens_per_s_layer": L / td,
+                    "speedup_vs_dense": td / t, "byte_bound_speedup": dense / alg,
+                    "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t / L) / 1e9})
+    del stack
+    torch.cuda.empty_cache()
+    return out
+
+
 def batch_kernels(ts, torch, fn, steps):
     res = {}
     for k in ("moe_router", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
@@ -509,7 +551,8 @@ def main():
     if args.workload == "mistral":
         print(json.dumps(run_mistral(args, ts, synth, torch)), flush=True)
         return
-    runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload, "given": run_given_workload}
+    runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload, "given": run_given_workload,
+            "act": run_act_workload}
     names = list(runs) if args.workload == "all" else [args.workload]
     for n in names:
         for r in runs[n](args, ts, synth, torch):
