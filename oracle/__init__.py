@@ -51,6 +51,8 @@ def _bind(lib):
     lib.or_ffn_given.restype = ctypes.c_int
     lib.or_ffn_act.argtypes = [vp, vp, vp, vp, ip, ip, ip, ip, ip, ctypes.c_double, dp, dp, dp, ip]
     lib.or_ffn_act.restype = ctypes.c_int
+    lib.or_ffn_topk.argtypes = [vp, vp, vp, vp, ip, ip, ip, ip, ip, dp, vp, ip]
+    lib.or_ffn_topk.restype = ctypes.c_int
     lib.or_max_threads.argtypes = []
     lib.or_max_threads.restype = ctypes.c_int
     return lib
@@ -175,6 +177,26 @@ def ffn_act(x, w_gate, w_up, w_down_t, dtype: int, act: int, tau: float = 0.0, t
     if rc != 0:
         raise RuntimeError("or_ffn_act failed")
     return ActResult(y=y, g=g, u=u, act=int(act), tau=float(tau))
+
+
+def ffn_topk(x, w_gate, w_up, w_down_t, dtype: int, keep: int, threads: int = 0, lib=None):
+    """dReLU FFN with the top-k magnitude mask in fp64: per token only the
+    `keep` largest |Combined| (ties: lower index) contribute.  Returns (y
+    [B][H], n_kept [B]: kept neurons with a non-zero activation)."""
+    lib = lib or _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    B, H = x.shape
+    wg, wu, wd = (_weights(w, dtype) for w in (w_gate, w_up, w_down_t))
+    I = wg.shape[0]
+    y = np.empty((B, H), np.float64)
+    nk = np.empty(B, np.int32)
+    rc = lib.or_ffn_topk(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), dtype, B, H, I, int(keep), _ptr(y), _ptr(nk),
+                         int(threads))
+    if rc != 0:
+        raise RuntimeError("or_ffn_topk failed")
+    return y, nk
 
 
 @dataclass

@@ -29,6 +29,7 @@
  * p = softmax(logits), S = the top_k experts by p (ties: lower index first),
  * w_e = p_e / sum_{e' in S} p_e', out = sum_{e in S, ascending e} w_e FFN_e(x).
  */
+#define _GNU_SOURCE
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -192,6 +193,81 @@ int or_ffn_act(const float *x, const void *wg, const void *wu, const void *wdt, 
         }
     }
     free(ha);
+    return 0;
+}
+
+/*
+ * The dReLU FFN with the top-k magnitude mask (section 3.2, Eq. mask and Eq.
+ * sparsify-gated-MLP): per token only the `keep` neurons with the largest
+ * |Combined| contribute (ties: the lower neuron index first; when keep
+ * exceeds the number of non-zero activations the extra kept neurons are
+ * zeros and change nothing):
+ *   y_t[j] = sum over kept i, ascending, of Combined_i * W_down_t[i][j].
+ *   n_kept [B] (nullable): kept neurons with a non-zero Combined activation.
+ * Returns 0, or -1 on bad arguments / allocation failure.
+ */
+static int cmp_desc_then_index(const void *pa, const void *pb, void *ctx)
+{
+    const double *h = (const double *)ctx;
+    int a = *(const int *)pa, b = *(const int *)pb;
+    double va = fabs(h[a]), vb = fabs(h[b]);
+    if (va > vb)
+        return -1;
+    if (va < vb)
+        return 1;
+    return (a > b) - (a < b);
+}
+
+int or_ffn_topk(const float *x, const void *wg, const void *wu, const void *wdt, int dtype, int B, int H, int I,
+                int keep, double *y, int32_t *n_kept, int nthreads)
+{
+    if (!x || !wg || !wu || !wdt || !y || B < 0 || H <= 0 || I < 0 || keep < 0 ||
+        (dtype != OR_F32 && dtype != OR_BF16))
+        return -1;
+    nthreads = set_threads(nthreads);
+    size_t nI = I > 0 ? (size_t)I : 1;
+    double *g = malloc(nI * sizeof *g), *u = malloc(nI * sizeof *u), *h = malloc(nI * sizeof *h);
+    double *hk = malloc(nI * sizeof *hk);
+    int *order = malloc(nI * sizeof *order);
+    if (!g || !u || !h || !hk || !order) {
+        free(g); free(u); free(h); free(hk); free(order);
+        return -1;
+    }
+    for (int t = 0; t < B; ++t) {
+        double *yt = y + (size_t)t * H;
+        /* Combined for every neuron (dReLU), then its dense sum is not used:
+           only the kept terms enter y. */
+        ffn_token(x + (size_t)t * H, wg, wu, wdt, dtype, H, I, yt, g, u, h, nthreads);
+        for (int i = 0; i < I; ++i)
+            order[i] = i;
+        qsort_r(order, (size_t)I, sizeof *order, cmp_desc_then_index, h);
+        int k = keep < I ? keep : I, nk = 0;
+        for (int i = 0; i < I; ++i)
+            hk[i] = 0.0;
+        for (int r = 0; r < k; ++r) {
+            hk[order[r]] = h[order[r]];
+            nk += h[order[r]] != 0.0;
+        }
+        if (n_kept)
+            n_kept[t] = nk;
+        int nblk = (H + 63) / 64;
+        int b;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+        for (b = 0; b < nblk; ++b) {
+            int j0 = b * 64, j1 = j0 + 64 < H ? j0 + 64 : H;
+            for (int j = j0; j < j1; ++j)
+                yt[j] = 0.0;
+            for (int ii = 0; ii < I; ++ii) {
+                double hv = hk[ii];
+                if (hv == 0.0)
+                    continue;
+                size_t row = (size_t)ii * (size_t)H;
+                for (int j = j0; j < j1; ++j)
+                    yt[j] += load_w(wdt, dtype, row + j) * hv;
+            }
+        }
+    }
+    free(g); free(u); free(h); free(hk); free(order);
     return 0;
 }
 

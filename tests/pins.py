@@ -446,7 +446,87 @@ def pin_act_drelu_is_dense_oracle(lib=None):
         raise AssertionError("dReLU with a threshold accepted")
 
 
+# ----------------------------------------------------------------------------
+# Top-k magnitude mask (Eq. mask / sparsify-gated-MLP)
+
+
+def _numpy_topk(inp, dtype, keep):
+    up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+    x = inp.x.astype(np.float64)
+    g = x @ up(inp.w_gate).astype(np.float64).T
+    u = x @ up(inp.w_up).astype(np.float64).T
+    h = np.where((g > 0) & (u > 0), g * u, 0.0)
+    wd = up(inp.w_down_t).astype(np.float64)
+    ys, nks = [], []
+    for t in range(h.shape[0]):
+        order = np.lexsort((np.arange(h.shape[1]), -np.abs(h[t])))[:keep]
+        kept = np.sort(order)
+        ys.append(h[t, kept] @ wd[kept] if kept.size else np.zeros(wd.shape[1]))
+        nks.append(int((h[t, kept] != 0).sum()))
+    return np.array(ys), np.array(nks), h
+
+
+def pin_topk_numpy(lib=None):
+    """The kept set and the masked sum against numpy (lexsort by |Combined|
+    descending, index ascending)."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(3, 128, 600, gate_bias=-0.3, dtype=dtype, seed=71)
+        for keep in (1, 17, 60, 250, 600, 900):
+            y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, keep, lib=lib)
+            yn, nkn, _ = _numpy_topk(inp, dtype, keep)
+            assert np.allclose(y, yn, rtol=1e-12, atol=1e-12 * max(np.abs(yn).max(), 1e-300)), (dtype, keep)
+            assert nk.tolist() == nkn.tolist()
+        y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, 0, lib=lib)
+        assert np.all(y == 0.0) and nk.tolist() == [0, 0, 0]
+
+
+def pin_topk_keep_all_is_dense(lib=None):
+    """Keeping at least every non-zero activation reproduces the dense oracle
+    bit for bit (the dropped terms are exact zeros); one fewer drops exactly
+    the smallest non-zero term."""
+    for dtype in (synth.F32, synth.BF16):
+        inp = synth.make_ffn(2, 96, 400, gate_bias=-0.84, dtype=dtype, seed=72)
+        rd = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, lib=lib)
+        na = int(rd.n_active.max())
+        for keep in (na, 400, 10 ** 6):
+            y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, dtype, keep, lib=lib)
+            if keep >= na:
+                assert np.array_equal(y.view(np.uint64), rd.y.view(np.uint64))
+                assert nk.tolist() == rd.n_active.tolist()
+        up = synth.bf16_bits_to_f32 if dtype == synth.BF16 else (lambda a: a)
+        t = 0
+        A = rd.active_set(t)
+        hv = rd.g[t, A] * rd.u[t, A]
+        small = A[np.argmin(hv)]
+        y, _ = oracle.ffn_topk(inp.x[:1], inp.w_gate, inp.w_up, inp.w_down_t, dtype, len(A) - 1, lib=lib)
+        term = up(inp.w_down_t)[small].astype(np.float64) * (rd.g[t, small] * rd.u[t, small])
+        assert np.allclose(y[0], rd.y[0] - term, rtol=1e-12, atol=1e-12 * np.abs(rd.y[0]).max())
+
+
+def pin_topk_ties_lower_index(lib=None):
+    """Neurons with identical weight rows have identical Combined values; a
+    cut through such a tie keeps the lower index."""
+    inp = synth.make_ffn(1, 64, 50, gate_bias=0.5, dtype=synth.F32, seed=73)
+    rd = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, synth.F32, lib=lib)
+    A = rd.active_set(0)
+    hv = rd.g[0, A] * rd.u[0, A]
+    top = A[np.argmax(hv)]
+    dup = [i for i in range(50) if i not in A][-1]   # an inactive neuron, becomes a copy of `top`
+    lo, hi = min(top, dup), max(top, dup)
+    for w in (inp.w_gate, inp.w_up):
+        w[dup] = w[top]
+    inp.w_down_t[dup] = synth.make_ffn(1, 64, 1, gate_bias=0.0, dtype=synth.F32, seed=74).w_down_t[0]
+    y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, synth.F32, 1, lib=lib)
+    r = oracle.ffn(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, synth.F32, lib=lib)
+    hlo = r.g[0, lo] * r.u[0, lo]
+    assert r.g[0, lo] * r.u[0, lo] == r.g[0, hi] * r.u[0, hi]
+    want = inp.w_down_t[lo].astype(np.float64) * hlo
+    assert np.array_equal(y[0], want), (lo, hi)
+    assert nk.tolist() == [1]
+
+
 ALL_PINS = [pin_ffn_handworked, pin_moe_handworked, pin_ffn_bruteforce, pin_moe_bruteforce,
             pin_ffn_zero_bias, pin_ffn_all_active_numpy, pin_ffn_sets_numpy, pin_ffn_skipzero_bitwise,
             pin_moe_special_cases, pin_given_bruteforce, pin_given_numpy, pin_given_exact_sets_bitwise,
-            pin_act_bruteforce, pin_act_numpy, pin_act_drelu_is_dense_oracle]
+            pin_act_bruteforce, pin_act_numpy, pin_act_drelu_is_dense_oracle, pin_topk_numpy,
+            pin_topk_keep_all_is_dense, pin_topk_ties_lower_index]

@@ -32,6 +32,10 @@ MUTANTS = {
     "act_unshifted_product": ("ha[i] = sg > tau ? (sg - tau) * su : 0.0;", "ha[i] = sg > tau ? sg * su : 0.0;"),
     "act_up_masked": ("ha[i] = sg > tau ? (sg - tau) * su : 0.0;",
                       "ha[i] = (sg > tau && su > 0.0) ? (sg - tau) * su : 0.0;"),
+    "topk_tie_upper_index": ("return (a > b) - (a < b);", "return (a < b) - (a > b);"),
+    "topk_smallest_first": ("    if (va > vb)\n        return -1;\n    if (va < vb)\n        return 1;",
+                            "    if (va > vb)\n        return 1;\n    if (va < vb)\n        return -1;"),
+    "topk_off_by_one": ("int k = keep < I ? keep : I, nk = 0;", "int k = keep < I ? keep + 1 : I, nk = 0;"),
     "given_gate_only_relu": ("hl[k] = (sg > 0.0 && su > 0.0) ? sg * su : 0.0;", "hl[k] = (sg > 0.0) ? sg * su : 0.0;"),
     "given_count_ignored": ("int n = count[t] < 0 ? 0 : (count[t] > maxc ? maxc : count[t]);", "int n = maxc;"),
     "given_down_list_position": ("double hv = hl[kk];\n                size_t row = (size_t)i * (size_t)H;",
