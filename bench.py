@@ -48,7 +48,7 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--workload", default="mistral",
-                    choices=["mistral", "sweep", "moe", "batch", "given", "act", "all"])
+                    choices=["mistral", "sweep", "moe", "batch", "given", "act", "topk", "all"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle CPU-baseline leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -395,6 +395,50 @@ def run_act_workload(args, ts, synth, torch):
     return out
 
 
+def run_topk_workload(args, ts, synth, torch):
+    """The top-k magnitude mask on the Mistral-shaped stack, batch 1
+    (ts_ffn_sparse_topk): keep 5% and 10% of the 14336 neurons per token
+    (about half, and about all, of dReLU's ~10% non-zero activations)."""
+    out = []
+    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
+    stack = Stack(ts, synth, L, 1, H, I, gate_bias=-0.8416, seed=5)
+    d = stack.data
+    td = timed(torch, stack.step_dense, args.steps, args.warmup)
+    f = ts.lib.ts_ffn_sparse_topk
+    for keep in (I // 20, I // 10):
+        counts = []
+        for l in range(L):
+            _, st = ts.ffn_sparse_topk(d["x"][l], d["w_gate"][l], d["w_up"][l], d["w_down_t"][l], keep,
+                                       stats=True)
+            torch.cuda.synchronize()
+            counts.append((int(st["n_gate"][0]), int(st["n_active"][0])))
+
+        def step():
+            for a in stack.args:
+                rc = f(*a[:8], keep, a[8], None, stack.ws.data_ptr(), stack.wsb, stack.stream)
+                if rc:
+                    raise RuntimeError(f"ts_ffn_sparse_topk -> {rc}")
+        t = timed(torch, step, args.steps, args.warmup)
+        kt = {}
+        for k in ("ffn_gate_up", "ffn_topk_select", "ffn_down", "ffn_reduce"):
+            n, ms = kernel_avg_ms(ts, torch, step, max(3, args.steps // 3), k)
+            if n:
+                kt[k + "_us"] = ms * 1e3
+        # gate rows whole, up rows of G, down rows of the kept set, x and out
+        alg = sum(2 * H * (I + ng + nk) + 8 * H for ng, nk in counts) / L
+        dense = 3 * 2 * H * I + 8 * H
+        out.append({"workload": "mistral7b_ffn_stack_bf16_b1_topk", "keep": keep,
+                    "gate_fraction": sum(c[0] for c in counts) / (L * I),
+                    "kept_fraction": sum(c[1] for c in counts) / (L * I),
+                    "sparse_tokens_per_s_layer": L / t, "dense_tokens_per_s_layer": L / td,
+                    "speedup_vs_dense": td / t, "byte_bound_speedup": dense / alg,
+                    "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t / L) / 1e9,
+                    "us_per_layer": t / L * 1e6, **kt})
+    del stack
+    torch.cuda.empty_cache()
+    return out
+
+
 def batch_kernels(ts, torch, fn, steps):
     res = {}
     for k in ("moe_router", "batch_prep", "batch_gate_up", "batch_down", "batch_reduce"):
@@ -552,7 +596,7 @@ def main():
         print(json.dumps(run_mistral(args, ts, synth, torch)), flush=True)
         return
     runs = {"sweep": run_sweep, "batch": run_batch_workload, "moe": run_moe_workload, "given": run_given_workload,
-            "act": run_act_workload}
+            "act": run_act_workload, "topk": run_topk_workload}
     names = list(runs) if args.workload == "all" else [args.workload]
     for n in names:
         for r in runs[n](args, ts, synth, torch):

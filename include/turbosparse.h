@@ -112,6 +112,22 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
                         ts_dtype wdtype, int batch, int hidden, int inter, float *out,
                         const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * The dReLU FFN with the top-k magnitude mask (section 3.2, Eq. mask and Eq.
+ * sparsify-gated-MLP, the paper's knob for measuring a model at a chosen
+ * sparsity): per token only the `keep` largest |Combined| activations enter
+ * the down projection (ties: the lower neuron index; keep above the number
+ * of non-zero activations keeps them all, i.e. the ts_ffn_sparse result).
+ * W_gate is read whole, the W_up rows of G and the W_down_t rows of the
+ * kept neurons only.  The activity report's A_t is the kept set (its
+ * non-zero members).  keep >= 0 (TS_ERR_SHAPE otherwise); inter <= 16384
+ * (TS_ERR_UNSUPPORTED otherwise: the per-token selection runs in on-chip
+ * memory).  Other arguments as ts_ffn_sparse, same workspace size.
+ */
+ts_status ts_ffn_sparse_topk(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                             ts_dtype wdtype, int batch, int hidden, int inter, int keep, float *out,
+                             const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
 /* Activation of the FFN (ts_ffn_sparse_act). */
 typedef enum {
     TS_ACT_DRELU = 0,     /* Eq. drelu: Combined = max(0, gate) * max(0, up) */

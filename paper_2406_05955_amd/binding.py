@@ -20,7 +20,7 @@ TS_BF16 = 1
 STATUS = {0: "TS_OK", 1: "TS_ERR_NULL", 2: "TS_ERR_SHAPE", 3: "TS_ERR_DTYPE", 4: "TS_ERR_ALIGN",
           5: "TS_ERR_WORKSPACE", 6: "TS_ERR_HIP", 7: "TS_ERR_UNSUPPORTED"}
 
-EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_sparse_act", "ts_ffn_dense",
+EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_sparse_act", "ts_ffn_sparse_topk", "ts_ffn_dense",
             "ts_ffn_given_workspace_bytes",
             "ts_ffn_sparse_given", "ts_moe_workspace_bytes", "ts_moe_sparse",
             "ts_moe_dense", "ts_status_str", "ts_last_error", "ts_version", "ts_prof_enable", "ts_prof_reset",
@@ -53,6 +53,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_ffn_dense.restype = st
     lib.ts_ffn_sparse_act.argtypes = [vp, vp, vp, vp, i, i, i, i, i, ctypes.c_float, vp, vp, vp, sz, vp]
     lib.ts_ffn_sparse_act.restype = st
+    lib.ts_ffn_sparse_topk.argtypes = [vp, vp, vp, vp, i, i, i, i, i, vp, vp, vp, sz, vp]
+    lib.ts_ffn_sparse_topk.restype = st
     lib.ts_ffn_given_workspace_bytes.argtypes = [i, i, i, i, i]
     lib.ts_ffn_given_workspace_bytes.restype = sz
     lib.ts_ffn_sparse_given.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, i, vp, vp, vp, sz, vp]
@@ -192,6 +194,24 @@ def ffn_sparse_act(x, w_gate, w_up, w_down_t, act: int, tau: float = 0.0, out=No
                                  float(tau), _ptr(out), ctypes.byref(st) if st is not None else None, _ptr(ws),
                                  ws.numel(), _stream(stream))
     _check(code, "ts_ffn_sparse_act")
+    return (out, d) if d is not None else out
+
+
+def ffn_sparse_topk(x, w_gate, w_up, w_down_t, keep: int, out=None, stats: bool = False, ws=None, stream=None):
+    """ts_ffn_sparse_topk: dReLU FFN keeping each token's `keep` largest
+    Combined activations.  Returns out, or (out, stats dict)."""
+    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    B, H = x.shape
+    I = w_gate.shape[0]
+    dt = wdtype_of(w_gate)
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    ws = _workspace(ffn_workspace_bytes(B, H, I, dt), x.device, ws)
+    st, d = _stats_struct(B, I, x.device, stats)
+    code = lib.ts_ffn_sparse_topk(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, int(keep),
+                                  _ptr(out), ctypes.byref(st) if st is not None else None, _ptr(ws), ws.numel(),
+                                  _stream(stream))
+    _check(code, "ts_ffn_sparse_topk")
     return (out, d) if d is not None else out
 
 

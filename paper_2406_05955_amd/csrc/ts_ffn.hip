@@ -106,6 +106,7 @@ struct SlotArgs {
     int32_t *gseg;           // [slots][ntiles][tile] tile's G, ascending (if want_seg)
     int32_t *aseg;           // [slots][ntiles][tile] tile's A, ascending (if want_seg)
     float *partial;          // [slots][ntiles][H]
+    float *hseg;             // [slots][ntiles][tile] Combined values of aseg (pipelined kernel, emit mode)
     int want_seg;
     // In-kernel routing (pipelined kernel, route == null): router weights
     // [E][H]; the tile-0 workgroup of each slot records its expert and
@@ -389,7 +390,10 @@ struct PipeWave {
     }
 };
 
-template <typename WT, int NC, int MR>
+// EMIT: stop after gate and up, writing each tile's A (ascending) with its
+// Combined values to aseg / hseg and |G|, |A| to cnt, for a kernel that
+// decides which of them enter the down projection (the top-k mask).
+template <typename WT, int NC, int MR, bool EMIT = false>
 __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     constexpr int CE = WTraits<WT>::CE;
     constexpr int NCD = (NC * 64 + kThreads - 1) / kThreads;
@@ -500,7 +504,8 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
                 const int pos = na0 + lane_prefix(ma, lane);
                 s_al[pos] = r;
                 s_av[pos] = s_h[r];
-                if (a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r;
+                if (EMIT || a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r;
+                if (EMIT) a.hseg[pr * a.tile + pos] = s_h[r];
             }
             ng += __popcll(mg);
             na0 += __popcll(ma);
@@ -512,6 +517,14 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     }
     __syncthreads();
     const int na = s_n[1];
+    if constexpr (EMIT) {
+        if (tid == 0) {
+            a.cnt[pr * 2] = s_n[0];
+            a.cnt[pr * 2 + 1] = na;
+        }
+        for (int q = na + tid; q < a.tile; q += kThreads) a.aseg[pr * a.tile + q] = -1;  // padding
+        return;
+    }
 
     // ---- down: axpy over the W_down_t rows of A, hidden split over threads --
     float acc[NCD][CE];
@@ -900,11 +913,237 @@ __global__ __launch_bounds__(kGateThreads) void ffn_gate_up(GateArgs a) {
             a.aseg[pr * a.tile + pos] = n0 + s_gl[lane];
             a.hseg[pr * a.tile + pos] = s_h[lane];
         }
+        if (lane >= __popcll(m) && lane < a.tile) a.aseg[pr * a.tile + lane] = -1;  // padding
         if (lane == 0) {
             a.cnt[pr * 2] = ng;
             a.cnt[pr * 2 + 1] = __popcll(m);
         }
     }
+}
+
+// Top-k magnitude mask (Eq. mask and Eq. sparsify-gated-MLP, section 3.2),
+// between gate+up and the down projection: per slot, keep the `keep`
+// largest Combined activations (all positive under dReLU, so |Combined| is
+// the value), ties to the lower neuron index, and rewrite each tile's active
+// list with the kept entries only, so the down kernel reads only their
+// W_down_t rows.  One 1024-thread workgroup per slot reads the padded
+// [ntiles][tile] lists (padding: index -1), whose positions run in
+// ascending neuron order:
+//   1. one batch of loads; the entries are compacted into LDS (one block
+//      scan) as key = (fp32 bits of the value) + 1 (order-preserving for
+//      non-negative floats, never 0), position and neuron index, and the
+//      first radix histogram is counted from registers;
+//   2. the k-th largest key by radix select over 8-bit digits, k =
+//      min(keep, entries) (histograms by LDS atomics: counts do not depend
+//      on order, so the result is deterministic; each bin search is one
+//      wave's suffix scan);
+//   3. when only some of the keys equal to the k-th are kept, the last kept
+//      position among them by a second radix select (over positions);
+//   4. kept flags set in a bitmap by position; each kept entry's place in
+//      its tile's list is the number of kept positions before it in the
+//      tile; the tiles' kept counts likewise.
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelPer = (kSelSpan + kSelThreads - 1) / kSelThreads;  // positions per thread
+
+struct SelArgs {
+    int ntiles, tile, keep;
+    const int32_t *cnt, *aseg;   // gate+up output: [slots][ntiles][2], [slots][ntiles][tile]
+    const float *hseg;
+    int32_t *kcnt, *kaseg;       // kept lists, same layout
+    float *khseg;
+};
+
+// Exclusive prefix over the workgroup of one int per thread; returns it, and
+// the total in *sum.  s_w: kSelWaves ints of scratch.  Contains barriers.
+__device__ __forceinline__ int sel_block_scan(int v, int *s_w, int *sum) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += t;
+    }
+    if (lane == 63) s_w[wave] = inc;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        const int t = s_w[w];
+        before += w < wave ? t : 0;
+        all += t;
+    }
+    __syncthreads();
+    *sum = all;
+    return before + inc - v;
+}
+
+// One radix step, run by wave 0: in the 256-bin histogram, the bin holding
+// the rem-th largest counted key (1 <= rem <= keys counted).  st[0] gains
+// the bin's digit at `shift`, st[1] becomes the rank left inside the bin,
+// st[2] the bin's count; the histogram is cleared for the next step.
+__device__ __forceinline__ void sel_find_bin(uint32_t *s_hist, uint32_t *st, uint32_t rem, int shift, int lane) {
+    uint32_t h[4], sum = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        h[j] = s_hist[4 * lane + j];
+        sum += h[j];
+    }
+    uint32_t inc = sum;  // bins of lanes >= this lane
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_down(inc, o, 64);
+        if (lane + o < 64) inc += t;
+    }
+    const uint32_t above = inc - sum;
+    if (above < rem && rem <= inc) {
+        uint32_t r = rem - above;
+        int j = 3;
+        for (; j > 0; --j) {
+            if (h[j] >= r) break;
+            r -= h[j];
+        }
+        st[0] |= (uint32_t)(4 * lane + j) << shift;
+        st[1] = r;
+        st[2] = h[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s_hist[4 * lane + j] = 0u;
+}
+
+// Kept positions in [lo, hi) of the bitmap.
+__device__ __forceinline__ int sel_bits(const uint32_t *s_kb, int lo, int hi) {
+    int c = 0;
+    for (int w = lo >> 5; lo < hi && w <= (hi - 1) >> 5; ++w) {
+        uint32_t m = s_kb[w];
+        if (w == lo >> 5) m &= ~0u << (lo & 31);
+        const int hb = hi - (w << 5);
+        if (hb < 32) m &= (1u << hb) - 1u;
+        c += __popc(m);
+    }
+    return c;
+}
+
+__global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
+    __shared__ uint32_t s_c[kSelMax];                 // entry keys (compacted)
+    __shared__ uint16_t s_cp[kSelMax];                // their list positions
+    __shared__ uint16_t s_ci[kSelMax];                // their neuron indices
+    __shared__ uint32_t s_kb[(kSelSpan + 31) / 32];   // kept flags by position
+    __shared__ uint32_t s_hist[256];
+    __shared__ int s_w[kSelWaves];
+    __shared__ uint32_t s_st[3];                      // digits found, rank left, bin count
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const size_t pr0 = (size_t)blockIdx.x * a.ntiles;
+    const int span = a.ntiles * a.tile;
+
+    // 1. staging
+    int n;
+    {
+        const uint32_t bytes = (uint32_t)span * 4u;
+        const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.hseg + pr0 * a.tile, bytes);
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.aseg + pr0 * a.tile, bytes);
+        uint32_t h[kSelPer], ai[kSelPer];
+#pragma unroll
+        for (int u = 0; u < kSelPer; ++u) {
+            const uint32_t off = (uint32_t)(tid + kSelThreads * u) * 4u;  // past `bytes`: zeros
+            h[u] = __builtin_amdgcn_raw_buffer_load_b32(rh, off, 0, 0);
+            ai[u] = __builtin_amdgcn_raw_buffer_load_b32(ra, off, 0, 0);
+        }
+        int ng[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int t = tid + kSelThreads * j;
+            ng[j] = t < a.ntiles ? a.cnt[(pr0 + t) * 2] : 0;
+        }
+        for (int i = tid; i < 256; i += kSelThreads) s_hist[i] = 0u;
+        for (int i = tid; i < (kSelSpan + 31) / 32; i += kSelThreads) s_kb[i] = 0u;
+        if (tid < 3) s_st[tid] = 0u;
+        int nv = 0;
+#pragma unroll
+        for (int u = 0; u < kSelPer; ++u) nv += (tid + kSelThreads * u < span && (int32_t)ai[u] >= 0) ? 1 : 0;
+        int base = sel_block_scan(nv, s_w, &n);  // its barriers also order the clears above
+#pragma unroll
+        for (int u = 0; u < kSelPer; ++u) {
+            const int e = tid + kSelThreads * u;
+            if (e < span && (int32_t)ai[u] >= 0) {
+                const uint32_t key = h[u] + 1u;
+                s_c[base] = key;
+                s_cp[base] = (uint16_t)e;
+                s_ci[base] = (uint16_t)ai[u];
+                ++base;
+                atomicAdd(&s_hist[key >> 24], 1u);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int t = tid + kSelThreads * j;
+            if (t < a.ntiles) a.kcnt[(pr0 + t) * 2] = ng[j];
+        }
+    }
+    const int k = min(a.keep, n);
+    __syncthreads();
+
+    // 2. the k-th largest key
+    uint32_t thr = 0xffffffffu;  // no key reaches it: nothing kept (k = 0)
+    uint32_t tie_pos = 0xffffu;  // last kept position among keys equal to thr
+    if (k > 0) {
+        uint32_t mask = 0u;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            if (shift < 24) {
+                const uint32_t prefix = s_st[0];
+                for (int i = tid; i < n; i += kSelThreads) {
+                    const uint32_t v = s_c[i];
+                    if ((v & mask) == prefix) atomicAdd(&s_hist[(v >> shift) & 255u], 1u);
+                }
+                __syncthreads();
+            }
+            if (wave == 0) sel_find_bin(s_hist, s_st, shift == 24 ? (uint32_t)k : s_st[1], shift, lane);
+            mask |= 255u << shift;
+            __syncthreads();
+        }
+        thr = s_st[0];
+        const uint32_t ties = s_st[1], neq = s_st[2];
+        // 3. only some of the keys equal to thr kept: the ties-th smallest
+        //    position among them (the ties-th largest of 0xffff - position)
+        if (ties < neq) {
+            __syncthreads();
+            if (tid == 0) s_st[0] = 0u;
+            __syncthreads();
+            mask = 0u;
+            for (int shift = 8; shift >= 0; shift -= 8) {
+                const uint32_t prefix = s_st[0];
+                for (int i = tid; i < n; i += kSelThreads) {
+                    const uint32_t q = 0xffffu - s_cp[i];
+                    if (s_c[i] == thr && (q & mask) == prefix) atomicAdd(&s_hist[(q >> shift) & 255u], 1u);
+                }
+                __syncthreads();
+                if (wave == 0) sel_find_bin(s_hist, s_st, shift == 8 ? ties : s_st[1], shift, lane);
+                mask |= 255u << shift;
+                __syncthreads();
+            }
+            tie_pos = 0xffffu - s_st[0];
+        }
+    }
+
+    // 4. kept flags by position, then the compacted per-tile lists
+    for (int i = tid; i < n; i += kSelThreads) {
+        const uint32_t v = s_c[i], pos = s_cp[i];
+        if (v > thr || (v == thr && pos <= tie_pos)) atomicOr(&s_kb[pos >> 5], 1u << (pos & 31));
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += kSelThreads) {
+        const int pos = s_cp[i];
+        if ((s_kb[pos >> 5] >> (pos & 31)) & 1u) {
+            const int t = pos / a.tile, lo = t * a.tile;
+            const size_t dst = (pr0 + t) * a.tile + sel_bits(s_kb, lo, pos);
+            a.kaseg[dst] = (int32_t)s_ci[i];
+            a.khseg[dst] = __uint_as_float(s_c[i] - 1u);
+        }
+    }
+    for (int t = tid; t < a.ntiles; t += kSelThreads)
+        a.kcnt[(pr0 + t) * 2 + 1] = sel_bits(s_kb, t * a.tile, (t + 1) * a.tile);
 }
 
 // Split path, kernel 2: the down projection over A.  Workgroup (slot, chunk,
@@ -1230,22 +1469,23 @@ void launch_fused_nc(int nc, int rif, dim3 grid, hipStream_t st, const SlotArgs 
 // The pipelined kernel keeps x, two gate rows and two up rows in registers;
 // with 128 x registers (NC = 16) it would spill, so wide rows use ffn_fused.
 // MR, the unrolled rows per wave, is the smallest of 2, 4, 8, 16 covering the tile.
-template <typename WT, int NC>
+template <typename WT, int NC, bool EMIT>
 void launch_pipe_mr(int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
     const int rows = (tile + kWaves - 1) / kWaves;
-    if (rows <= 2) launch("ffn_main", ffn_pipe<WT, NC, 2>, grid, dim3(kThreads), st, a);
-    else if (rows <= 4) launch("ffn_main", ffn_pipe<WT, NC, 4>, grid, dim3(kThreads), st, a);
-    else if (rows <= 8) launch("ffn_main", ffn_pipe<WT, NC, 8>, grid, dim3(kThreads), st, a);
-    else launch("ffn_main", ffn_pipe<WT, NC, 16>, grid, dim3(kThreads), st, a);
+    const char *name = EMIT ? "ffn_gate_up" : "ffn_main";
+    if (rows <= 2) launch(name, ffn_pipe<WT, NC, 2, EMIT>, grid, dim3(kThreads), st, a);
+    else if (rows <= 4) launch(name, ffn_pipe<WT, NC, 4, EMIT>, grid, dim3(kThreads), st, a);
+    else if (rows <= 8) launch(name, ffn_pipe<WT, NC, 8, EMIT>, grid, dim3(kThreads), st, a);
+    else launch(name, ffn_pipe<WT, NC, 16, EMIT>, grid, dim3(kThreads), st, a);
 }
 
-template <typename WT>
+template <typename WT, bool EMIT = false>
 void launch_pipe(int nc, int tile, dim3 grid, hipStream_t st, const SlotArgs &a) {
     switch (nc) {
-    case 1: launch_pipe_mr<WT, 1>(tile, grid, st, a); break;
-    case 2: launch_pipe_mr<WT, 2>(tile, grid, st, a); break;
-    case 4: launch_pipe_mr<WT, 4>(tile, grid, st, a); break;
-    default: launch_pipe_mr<WT, 8>(tile, grid, st, a); break;
+    case 1: launch_pipe_mr<WT, 1, EMIT>(tile, grid, st, a); break;
+    case 2: launch_pipe_mr<WT, 2, EMIT>(tile, grid, st, a); break;
+    case 4: launch_pipe_mr<WT, 4, EMIT>(tile, grid, st, a); break;
+    default: launch_pipe_mr<WT, 8, EMIT>(tile, grid, st, a); break;
     }
 }
 
@@ -1329,10 +1569,29 @@ ts_status run_report(const SlotPlan &p, const int32_t *cnt, const int32_t *gseg,
     return TS_OK;
 }
 
+// The top-k selection over lists of `ntiles` tiles of `tile` entries per
+// slot, into the workspace's kept lists (off_kcnt / off_kaseg / off_khseg).
+ts_status launch_select(const SlotPlan &p, int ntiles, int tile, int keep, const int32_t *cnt, const int32_t *aseg,
+                        const float *hseg, void *ws, hipStream_t st) {
+    SelArgs sa;
+    sa.ntiles = ntiles;
+    sa.tile = tile;
+    sa.keep = keep;
+    sa.cnt = cnt;
+    sa.aseg = aseg;
+    sa.hseg = hseg;
+    sa.kcnt = ws_at<int32_t>(ws, p.off_kcnt);
+    sa.kaseg = ws_at<int32_t>(ws, p.off_kaseg);
+    sa.khseg = ws_at<float>(ws, p.off_khseg);
+    launch("ffn_topk_select", ffn_topk_select, dim3((unsigned)p.slots), dim3(kSelThreads), st, sa);
+    return check_launch("ffn_topk_select");
+}
+
 // Split sparse path over `p.slots` slots: gate+up, down, reduce, report.
+// keep >= 0: the top-k magnitude mask between the two kernels.
 ts_status run_split(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
                     size_t expert_stride, ts_dtype dt, const SlotPlan &p, float *out, const float *slot_w,
-                    const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+                    const ts_ffn_stats *stats, void *ws, hipStream_t st, int keep = -1) {
     const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
     GateArgs g;
     g.x = x;
@@ -1358,6 +1617,13 @@ ts_status run_split(const float *x, const void *wg, const void *wu, const void *
     }
     ts_status s = check_launch("ffn_gate_up");
     if (s != TS_OK) return s;
+    if (keep >= 0) {
+        s = launch_select(p, p.gntiles, p.gtile, keep, g.cnt, g.aseg, g.hseg, ws, st);
+        if (s != TS_OK) return s;
+        g.cnt = ws_at<int32_t>(ws, p.off_kcnt);
+        g.aseg = ws_at<int32_t>(ws, p.off_kaseg);
+        g.hseg = ws_at<float>(ws, p.off_khseg);
+    }
     DownArgs d;
     d.wd = wd;
     d.route = route;
@@ -1399,7 +1665,7 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
                     const float *slot_w, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool pipe,
                     const RouterFold *rf = nullptr, int act = 0, float tau = 0.f) {
     const bool want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union);
-    SlotArgs a;
+    SlotArgs a{};
     a.act = act;
     a.tau = tau;
     a.wr = rf ? rf->wr : nullptr;
@@ -1448,6 +1714,64 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
 // The kernel sequence run_slots picks: the pipelined kernel unless the dense
 // comparator, a tuning knob or a row too wide for it asks for another.
 bool slots_use_pipe(const SlotPlan &p, bool dense) { return !dense && tuned("ffn_path") == 0 && p.nc <= 8; }
+
+// The top-k mask over single-token slots (the FFN's tokens): the pipelined
+// kernel in emit mode (gate and up at its streaming rate), the selection,
+// the split path's down kernel over the kept lists, reduce, report.  Rows
+// too wide for the pipelined kernel take the split path's gate+up kernel.
+ts_status run_topk(const float *x, const void *wg, const void *wu, const void *wd, ts_dtype dt, const SlotPlan &p,
+                   float *out, const ts_ffn_stats *stats, void *ws, hipStream_t st, int keep) {
+    if (!slots_use_pipe(p, false))
+        return run_split(x, wg, wu, wd, nullptr, 0, dt, p, out, nullptr, stats, ws, st, keep);
+    SlotArgs a{};
+    a.x = x;
+    a.wg = wg;
+    a.wu = wu;
+    a.wd = wd;
+    a.H = p.hidden;
+    a.I = p.inter;
+    a.tile = p.tile;
+    a.ntiles = p.ntiles;
+    a.slots_per_tok = 1;
+    a.cnt = ws_at<int32_t>(ws, p.off_cnt);
+    a.gseg = ws_at<int32_t>(ws, p.off_gseg);
+    a.aseg = ws_at<int32_t>(ws, p.off_aseg);
+    a.hseg = ws_at<float>(ws, p.off_hseg);
+    a.partial = ws_at<float>(ws, p.off_partial);
+    a.want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union) ? 1 : 0;
+    const dim3 grid((unsigned)(p.slots * p.ntiles));
+    if (dt == TS_F32) launch_pipe<float, true>(p.nc, p.tile, grid, st, a);
+    else launch_pipe<uint16_t, true>(p.nc, p.tile, grid, st, a);
+    ts_status s = check_launch("ffn_gate_up");
+    if (s != TS_OK) return s;
+    s = launch_select(p, p.ntiles, p.tile, keep, a.cnt, a.aseg, a.hseg, ws, st);
+    if (s != TS_OK) return s;
+    DownArgs d;
+    d.wd = wd;
+    d.route = nullptr;
+    d.expert_stride = 0;
+    d.H = p.hidden;
+    d.tile = p.tile;
+    d.ntiles = p.ntiles;
+    d.nslices = p.nslices;
+    d.nchunks = p.pnchunks;
+    d.tpc = p.ptpc;
+    d.cnt = ws_at<int32_t>(ws, p.off_kcnt);
+    d.aseg = ws_at<int32_t>(ws, p.off_kaseg);
+    d.hseg = ws_at<float>(ws, p.off_khseg);
+    d.partial = a.partial;
+    {
+        dim3 dg((unsigned)(p.slots * p.pnchunks * p.nslices));
+        if (dt == TS_F32) launch("ffn_down", ffn_down<float>, dg, dim3(kDownThreads), st, d);
+        else launch("ffn_down", ffn_down<uint16_t>, dg, dim3(kDownThreads), st, d);
+    }
+    s = check_launch("ffn_down");
+    if (s != TS_OK) return s;
+    s = launch_reduce(d.partial, p.pnchunks, p, nullptr, out, st);
+    if (s != TS_OK) return s;
+    return run_report(p, d.cnt, a.gseg, d.aseg, p.ntiles, p.tile, stats, ws, st);
+}
+
 
 // `rf` (pipelined kernel only, route == null) moves the MoE router into it.
 ts_status run_slots(const float *x, const void *wg, const void *wu, const void *wd, const int32_t *route,
@@ -1571,6 +1895,21 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
         return TS_OK;
     }
     return ts::run_slots(x, w_gate, w_up, w_down_t, nullptr, 0, wdtype, false, p, out, nullptr, stats, ws, st);
+}
+
+ts_status ts_ffn_sparse_topk(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                             ts_dtype wdtype, int batch, int hidden, int inter, int keep, float *out,
+                             const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream) {
+    if (keep < 0) return TS_ERR_SHAPE;
+    ts::SlotPlan p;
+    ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws,
+                                     ws_bytes, &p);
+    if (s != TS_OK) return s;
+    if (inter > ts::kSelMax || p.gntiles * p.gtile > ts::kSelSpan || p.ntiles * p.tile > ts::kSelSpan ||
+        p.gntiles > ts::kSelMaxTiles || p.ntiles > ts::kSelMaxTiles)
+        return TS_ERR_UNSUPPORTED;
+    return ts::run_topk(x, w_gate, w_up, w_down_t, wdtype, p, out, stats, ws, static_cast<hipStream_t>(stream),
+                        keep);
 }
 
 ts_status ts_ffn_sparse_act(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,

@@ -108,6 +108,8 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     off = align256(off + nseg * sizeof(int32_t));
     q.off_aseg = off;
     off = align256(off + nseg * sizeof(int32_t));
+    q.off_hseg = off;
+    off = align256(off + nseg * sizeof(float));
     q.off_partial = off;
     off = align256(off + nst * (size_t)hidden * sizeof(float));
     q.off_route_idx = off;
@@ -138,6 +140,15 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     tpc = std::min(tpc, std::min(kDownMaxTiles, kDownMaxRows / gt));
     q.tpc = std::max(1, tpc);
     q.nchunks = (q.gntiles + q.tpc - 1) / q.tpc;
+    {
+        // the same decomposition over the pipelined kernel's tiles (its
+        // partial rows go to off_partial, which holds one per tile)
+        int pn = std::max(1, std::min(want, q.ntiles));
+        int ptpc = (q.ntiles + pn - 1) / pn;
+        ptpc = std::min(ptpc, std::min(kDownMaxTiles, kDownMaxRows / q.tile));
+        q.ptpc = std::max(1, ptpc);
+        q.pnchunks = (q.ntiles + q.ptpc - 1) / q.ptpc;
+    }
     size_t gst = (size_t)slots * (size_t)q.gntiles;
     q.off_gcnt = off;
     off = align256(off + gst * 2 * sizeof(int32_t));
@@ -151,6 +162,14 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     off = align256(off + (size_t)slots * q.nchunks * (size_t)hidden * sizeof(float));
     q.off_ctr = off;
     off = align256(off + (size_t)q.outs * q.nslices * sizeof(int32_t));
+    const size_t kst = std::max(gst, (size_t)slots * (size_t)q.ntiles);
+    const size_t kseg = std::max(gst * (size_t)gt, (size_t)slots * (size_t)q.ntiles * q.tile);
+    q.off_kcnt = off;
+    off = align256(off + kst * 2 * sizeof(int32_t));
+    q.off_kaseg = off;
+    off = align256(off + kseg * sizeof(int32_t));
+    q.off_khseg = off;
+    off = align256(off + kseg * sizeof(float));
     q.total = off;
     *p = q;
     return true;

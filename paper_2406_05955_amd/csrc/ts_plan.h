@@ -25,6 +25,9 @@ constexpr int kDownThreads = 256;         // 4 waves per down workgroup
 constexpr int kDownMaxRows = 1024;        // active rows one down workgroup can list in LDS
 constexpr int kDownTargetBlocks = 256;
 constexpr int kDownMaxTiles = 256;        // gate+up tiles one down workgroup can list
+constexpr int kSelMax = 16384;            // Combined values the top-k selection holds in LDS (inter limit)
+constexpr int kSelMaxTiles = 2048;        // gate+up tiles per slot the selection lists (inter / 8)
+constexpr int kSelSpan = kSelMax + 128;   // padded list positions per slot it holds (last tile's padding)
 
 // Workspace layout and launch shape shared by the single-token path (one
 // "slot" = one (token, expert) pair processed against one weight set).
@@ -46,10 +49,15 @@ struct SlotPlan {
     int nslices = 0;   // column slices of the down kernel (64 chunks of 16 bytes each)
     int nchunks = 0;   // groups of gate+up tiles per slot in the down kernel
     int tpc = 0;       // gate+up tiles per chunk
+    int pnchunks = 0;  // the down kernel over the pipelined kernel's tiles (top-k mask): chunks per slot
+    int ptpc = 0;      // and pipelined tiles per chunk
     // byte offsets into the workspace
     size_t off_cnt = 0, off_gseg = 0, off_aseg = 0, off_partial = 0;
     size_t off_route_idx = 0, off_route_w = 0, off_aux = 0;
     size_t off_gcnt = 0, off_ggseg = 0, off_gaseg = 0, off_ghseg = 0, off_dpartial = 0, off_ctr = 0;
+    size_t off_hseg = 0;  // Combined values of aseg (pipelined kernel's emit mode)
+    // the top-k mask's kept lists (either kernel's tile layout)
+    size_t off_kcnt = 0, off_kaseg = 0, off_khseg = 0;
     size_t total = 0;
 };
 

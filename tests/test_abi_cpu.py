@@ -166,3 +166,16 @@ def test_act_checks():
     assert call(wsb=need - 1) == WS
     assert call(act=0, wsb=need - 1) == WS
     assert call(B=0) == SHAPE
+
+
+def test_topk_checks():
+    f = ts.lib.ts_ffn_sparse_topk
+
+    def call(keep=100, B=1, H=4096, I=14336, out=A, ws=A, wsb=1 << 40, stats=None):
+        return f(A, A, A, A, 1, B, H, I, keep, out, stats, ws, wsb, None)
+    assert call(keep=-1) == SHAPE
+    assert call(I=16385) == UNSUP
+    assert call(out=A + 8) == ALIGN
+    need = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
+    assert call(wsb=need - 1) == WS
+    assert call(B=0) == SHAPE
