@@ -277,6 +277,10 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *                batches in flight), 1 = 2 x 2, 2 = 2 x 4
  *   "bx_down"    batched down kernel for up to 16 tokens per group: 0 default
  *                (2 blocks of 32 rows in flight per wave), 1 = 3 blocks
+ *   "bx_vgroup"  batched MoE layer: 0 default (token slots per expert group
+ *                about twice the expected expert load; an expert with more
+ *                tokens takes further groups), 1 = one group per expert
+ *                with slots for the whole batch
  * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
  */
 ts_status ts_tune_set(const char *key, int value);

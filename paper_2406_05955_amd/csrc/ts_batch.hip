@@ -82,6 +82,7 @@ struct BxArgs {
     const void *wg, *wu, *wd;
     size_t expert_stride;    // elements per expert matrix (0: one weight set)
     int B, H, I, G, K, bpad, hpad, ntiles, nslices, nchunks, tpc;
+    int vpe;                 // groups per weight set: group g uses weight set g / vpe
     const int32_t *topk;     // [B][K] routed experts, or null (FFN)
     const float *topw;       // [B][K] routing weights, or null
     int32_t *gcount;         // [G]
@@ -120,16 +121,18 @@ __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
     const int g = (blockIdx.x * 4) / (NX * nks);
     const bool first = blockIdx.x * 4 == g * NX * nks;
     if (a.topk) {
+        // group g holds entries [r0, r0 + TOK) of expert g / vpe's list
         if (threadIdx.x < 64) {
             const int lane = threadIdx.x;
             const int np = a.B * a.K;
+            const int e = g / a.vpe, r0 = (g - e * a.vpe) * TOK;
             int base = 0;
             for (int p0 = 0; p0 < np; p0 += 64) {
                 const int p = p0 + lane;
-                const bool mine = p < np && a.topk[p] == g;
+                const bool mine = p < np && a.topk[p] == e;
                 const uint64_t m = __ballot(mine);
-                if (mine) {
-                    const int rank = base + lane_prefix(m, lane);  // < TOK: top-k experts are distinct
+                const int rank = base + lane_prefix(m, lane) - r0;  // rank within this group
+                if (mine && rank >= 0 && rank < TOK) {
                     s_tok[rank] = p / a.K;
                     if (first) {
                         a.tslot[p * 2] = g;
@@ -138,8 +141,9 @@ __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
                 }
                 base += __popcll(m);
             }
-            for (int sl = base + lane; sl < TOK; sl += 64) s_tok[sl] = -1;
-            if (first && lane == 0) a.gcount[g] = base;
+            const int n = min(max(base - r0, 0), TOK);
+            for (int sl = n + lane; sl < TOK; sl += 64) s_tok[sl] = -1;
+            if (first && lane == 0) a.gcount[g] = n;
         }
         __syncthreads();
     } else if (blockIdx.x == 0) {
@@ -382,8 +386,8 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
         reinterpret_cast<u32x4 *>(&s_h[0][0])[e] = u32x4{0u, 0u, 0u, 0u};
 
     const int r0 = tile * kBxRows;
-    const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)g * a.expert_stride;
-    const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)g * a.expert_stride;
+    const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)(g / a.vpe) * a.expert_stride;
+    const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)(g / a.vpe) * a.expert_stride;
     const int nks = a.hpad / 32;
     const u32x4 *xg = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * nks * NX * 64;
     const int kpw = nks / 4;  // k-steps per wave
@@ -605,7 +609,7 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     }
     __syncthreads();
 
-    const char *wd = reinterpret_cast<const char *>(reinterpret_cast<const uint16_t *>(a.wd) + (size_t)g * a.expert_stride);
+    const char *wd = reinterpret_cast<const char *>(reinterpret_cast<const uint16_t *>(a.wd) + (size_t)(g / a.vpe) * a.expert_stride);
     const int col0 = slice * kBxSliceCols;
     const uint32_t cw = 2u * (uint32_t)min(col0 + 8 * lm, H - 8);
     const uint32_t H2 = 2u * (uint32_t)H;
@@ -895,6 +899,7 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     a.H = p.hidden;
     a.I = p.inter;
     a.G = p.groups;
+    a.vpe = p.vpe;
     a.K = p.top_k;
     a.bpad = p.bpad;
     a.hpad = p.hpad;

@@ -16,6 +16,7 @@ std::atomic<int> g_rif{0};
 std::atomic<int> g_batch{0};
 std::atomic<int> g_bx_gate{0};
 std::atomic<int> g_bx_down{0};
+std::atomic<int> g_bx_vgroup{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
@@ -34,6 +35,7 @@ int tuned(const char *key) {
     if (std::strcmp(key, "batch_path") == 0) return g_batch.load();
     if (std::strcmp(key, "bx_gate") == 0) return g_bx_gate.load();
     if (std::strcmp(key, "bx_down") == 0) return g_bx_down.load();
+    if (std::strcmp(key, "bx_vgroup") == 0) return g_bx_vgroup.load();
     return 0;
 }
 
@@ -175,8 +177,8 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     return true;
 }
 
-bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p) {
-    if (check_dims(batch, hidden, inter, dt) != TS_OK || dt != TS_BF16 || groups < 1 || top_k < 1) return false;
+bool plan_batch(int batch, int hidden, int inter, int experts, int top_k, ts_dtype dt, BatchPlan *p) {
+    if (check_dims(batch, hidden, inter, dt) != TS_OK || dt != TS_BF16 || experts < 1 || top_k < 1) return false;
     if (batch > kBxMaxTokens) return false;
     // the gate / up kernel addresses rows with 32-bit byte offsets into one matrix
     if ((unsigned long long)inter * (unsigned long long)hidden * 2ull >= (1ull << 32)) return false;
@@ -184,10 +186,18 @@ bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtyp
     q.batch = batch;
     q.hidden = hidden;
     q.inter = inter;
-    q.groups = groups;
     q.top_k = top_k;
-    // token slots per group: the kernels are built for 8, 16, 32 and 64
-    q.tok = batch <= 8 ? 8 : (batch <= 16 ? 16 : (batch <= 32 ? 32 : 64));
+    q.experts = experts;
+    // token slots per group (the kernels are built for 8, 16, 32 and 64):
+    // the batch for one weight set; for several, twice an expert's expected
+    // load batch * top_k / experts (the "bx_vgroup" knob 1: the batch)
+    int slots = batch;
+    if (experts > 1 && g_bx_vgroup.load() == 0)
+        slots = std::min(batch, 2 * ((batch * top_k + experts - 1) / experts));
+    q.tok = slots <= 8 ? 8 : (slots <= 16 ? 16 : (slots <= 32 ? 32 : 64));
+    q.vpe = (batch + q.tok - 1) / q.tok;  // an expert holds each token at most once
+    q.groups = experts * q.vpe;
+    const int groups = q.groups;
     q.bpad = q.tok;
     q.hpad = (hidden + kBxKQuant - 1) / kBxKQuant * kBxKQuant;
     q.ntiles = (inter + kBxRows - 1) / kBxRows;
@@ -361,6 +371,11 @@ ts_status ts_tune_set(const char *key, int value) {
     if (std::strcmp(key, "bx_down") == 0) {
         if (value < 0 || value > 1) return TS_ERR_SHAPE;
         ts::g_bx_down.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "bx_vgroup") == 0) {
+        if (value < 0 || value > 1) return TS_ERR_SHAPE;
+        ts::g_bx_vgroup.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;

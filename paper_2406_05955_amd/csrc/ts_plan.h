@@ -72,8 +72,16 @@ constexpr int kBxSliceCols = 128; // output columns per down wave
 constexpr int kBxChunkTiles = 64; // gate+up tiles per down chunk (one wave ballot)
 constexpr int kBxKQuant = 1024;   // the hidden dimension is padded to this (4 waves x 2 batches x 128)
 
+// A "group" is one weight set with up to `tok` of its tokens.  The FFN has
+// one group holding the batch.  In the MoE layer each expert's token list
+// (known only on the device) is cut into `vpe` groups of `tok` consecutive
+// entries, with tok about twice the expected load of an expert: an expert
+// that draws more tokens than that takes a second group (its weights are
+// read once more), and a group that draws none exits at once.
 struct BatchPlan {
     int batch = 0, hidden = 0, inter = 0, groups = 1, top_k = 1;
+    int experts = 1;     // weight sets
+    int vpe = 1;         // groups per weight set (groups = experts * vpe)
     int tok = 0;         // token slots per group: 8 (high / low x parts share one MFMA tile), 16, 32 or 64
     int bpad = 0;        // = tok
     int hpad = 0;        // hidden rounded up to kBxKQuant (gate / up K range, zero x past hidden)

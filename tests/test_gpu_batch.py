@@ -130,7 +130,28 @@ def test_moe_batch_shapes(B, H, I, E, K):
     moe_check(m)
 
 
-@pytest.mark.parametrize("B", [16, 32])
+def test_moe_batch_overflow_groups():
+    """Token slots per expert group are sized for about twice the expected
+    expert load; a router that sends every token to experts 0 and 1 makes
+    both take further groups (each reads its weights once per group)."""
+    B, H, I, E, K = 32, 1024, 1500, 8, 2
+    m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=synth.BF16, seed=36)
+    m.w_router[0, 0] = synth.f32_to_bf16_bits(np.float32([10.0]))[0]  # x[:, 0] = 1: a logit bias
+    m.w_router[1, 0] = synth.f32_to_bf16_bits(np.float32([9.0]))[0]
+    ref, out = moe_check(m)
+    assert (np.sort(ref.topk_idx, axis=1) == [0, 1]).all()
+    # one group per expert with slots for the whole batch: same result up to summation order
+    ts.tune_set("bx_vgroup", 1)
+    try:
+        out1 = ts.moe_sparse(to_dev(m.x), to_dev(m.w_router), to_dev(m.w_gate), to_dev(m.w_up),
+                             to_dev(m.w_down_t), K)[0]
+        torch.cuda.synchronize()
+    finally:
+        ts.tune_set("bx_vgroup", 0)
+    assert rel_l2(out.cpu().numpy(), out1.cpu().numpy()) <= 1e-5
+
+
+@pytest.mark.parametrize("B", [16, 32, 64])
 def test_moe_batch_mixtral_shape(B):
     L = synth.make_moe_stack_torch(1, B, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=3,
                                    device=DEV)
