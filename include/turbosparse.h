@@ -269,13 +269,14 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *                1 = single-token kernels per token
  *   "gate_tile"  neurons per workgroup of the split path's gate+up kernel
  *                (4..64, multiple of 4)
- *   "down_chunks" tile groups per slot in the split path's down kernel
+ *   "down_chunks" tile groups per slot in the split path's down kernel, and
+ *                per group in the batched down kernel
  *   "rif"        weight rows in flight per wave in the row dot products
  *                (1 or 2)
  *   "bx_gate"    load shape of the batched gate+up kernel for up to 16
  *                tokens per group: 0 default (4 k-steps of 32 per batch, 2
  *                batches in flight), 1 = 2 x 2, 2 = 2 x 4
- *   "bx_down"    batched down kernel for up to 16 tokens per group: 0 default
+ *   "bx_down"    batched down kernel for up to 32 tokens per group: 0 default
  *                (2 blocks of 32 rows in flight per wave), 1 = 3 blocks
  *   "bx_vgroup"  batched MoE layer: 0 default (token slots per expert group
  *                about twice the expected expert load; an expert with more

@@ -547,9 +547,11 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
 // conflict.  The block's Combined values (slot-major records written by
 // bx_gate_up) are transposed through a small LDS tile into the other
 // operand (token rows, 8 consecutive slots per lane).  Slots past the last
-// row repeat a listed row with zero Combined.  Loads of the next DD - 1
+// row load zeros (out-of-range buffer offset) with zero Combined.  Loads of the next DD - 1
 // blocks are in flight while a block is contracted; the four waves' sums
 // are added in a fixed order at the end.
+constexpr uint32_t kPadRow = 0xFFFFFFFFu;  // row-list padding of bx_down
+
 template <int TOK, int DD>
 __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     using S = Bx<TOK>;
@@ -579,7 +581,15 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     const int ntc = min(a.tpc, a.ntiles - t0);
     const size_t tbase = (size_t)g * a.ntiles + t0;
 
-    // ---- the chunk's row list ---------------------------------------------
+    // ---- the chunk's row list: the tiles' counts and row bytes are read in
+    // one round trip (bx_gate_up writes all 32 row bytes of a tile) ---------
+    constexpr int EPT = MAXR / 256;  // tile entries per thread
+    uint32_t rbv[EPT];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+        const int e = tid + 256 * u;
+        rbv[u] = e < ntc * kBxRows ? a.arow[tbase * kBxRows + e] : 0u;
+    }
     if (wave == 0) {
         const int na = lane < ntc ? a.cnt[(tbase + lane) * 2 + 1] : 0;
         int inc = na;
@@ -593,23 +603,29 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     }
     __syncthreads();
     const int total = s_pre[ntc];
-    for (int e = tid; e < ntc * kBxRows; e += 256) {
-        const int t = e / kBxRows, sl = e % kBxRows;
-        const int base = s_pre[t];
-        if (sl < s_pre[t + 1] - base) {
-            s_row[base + sl] = (uint32_t)((t0 + t) * kBxRows + a.arow[(tbase + t) * kBxRows + sl]);
-            s_hix[base + sl] = (int32_t)((tbase + t) * kBxRows + sl);
-        }
-    }
     const int nblk = (total + kBxRows - 1) / kBxRows;
-    __syncthreads();
-    for (int e = total + tid; e < nblk * kBxRows; e += 256) {
-        s_row[e] = s_row[0];
-        s_hix[e] = -1;
+    // listed rows; the block padding past `total` loads at an out-of-range
+    // offset (zeros, no traffic) and has zero Combined
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+        const int e = tid + 256 * u;
+        if (e < ntc * kBxRows) {
+            const int t = e / kBxRows, sl = e - t * kBxRows;
+            const int base = s_pre[t];
+            if (sl < s_pre[t + 1] - base) {
+                s_row[base + sl] = (uint32_t)((t0 + t) * kBxRows) + rbv[u];
+                s_hix[base + sl] = (int32_t)((tbase + t) * kBxRows + sl);
+            }
+        }
+        if (e >= total && e < nblk * kBxRows) {
+            s_row[e] = kPadRow;
+            s_hix[e] = -1;
+        }
     }
     __syncthreads();
 
-    const char *wd = reinterpret_cast<const char *>(reinterpret_cast<const uint16_t *>(a.wd) + (size_t)(g / a.vpe) * a.expert_stride);
+    const uint16_t *wde = reinterpret_cast<const uint16_t *>(a.wd) + (size_t)(g / a.vpe) * a.expert_stride;
+    const __amdgpu_buffer_rsrc_t rwd = make_rsrc(wde, (uint32_t)a.I * (uint32_t)H * 2u);
     const int col0 = slice * kBxSliceCols;
     const uint32_t cw = 2u * (uint32_t)min(col0 + 8 * lm, H - 8);
     const uint32_t H2 = 2u * (uint32_t)H;
@@ -636,7 +652,8 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
             const u32x4 rb = *reinterpret_cast<const u32x4 *>(&s_row[bb * kBxRows + 8 * lq + 4]);
             const uint32_t rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-            for (int q = 0; q < 8; ++q) wv[d][q] = ld_stream(wd + (rr[q] * H2 + cw));
+            for (int q = 0; q < 8; ++q)
+                wv[d][q] = ld_buf_stream(rwd, rr[q] == kPadRow ? kOutOfRange : rr[q] * H2 + cw);
             const int hx = s_hix[bb * kBxRows + hj];
             hok[d] = hx >= 0;
             const uint16_t *hs = a.hfrag + (size_t)(hx >= 0 ? hx : 0) * (2 * TOK) + hh * TOK;
@@ -855,7 +872,7 @@ T *ws_at(void *ws, size_t off) {
 template <int TOK>
 void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
     const dim3 grid((unsigned)(p.groups * p.ntiles));
-    if constexpr (TOK <= 16) {
+    if constexpr (TOK <= 16) {  // deeper shapes spill registers at 32 tokens and run slower
         switch (tuned("bx_gate")) {
         case 1: launch("batch_gate_up", bx_gate_up<TOK, 2, 2>, grid, dim3(256), st, a); return;
         case 2: launch("batch_gate_up", bx_gate_up<TOK, 2, 4>, grid, dim3(256), st, a); return;
@@ -871,7 +888,7 @@ void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
     launch("batch_prep", bx_prep<TOK>, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), st, a);
     launch_gate_up<TOK>(p, a, st);
     const dim3 grid((unsigned)(p.groups * p.nchunks * p.nslices));
-    if constexpr (TOK <= 16) {
+    if constexpr (TOK <= 32) {
         if (tuned("bx_down") == 1) {
             launch("batch_down", bx_down<TOK, 3>, grid, dim3(256), st, a);
             return;

@@ -129,30 +129,53 @@ __device__ __forceinline__ float combined_value(int act, float tau, float g, flo
     return act ? (g - tau) * u : g * u;
 }
 
-// Softmax over the E logits, the top K (strictly larger wins, so the lower
-// index wins exact ties) and their renormalised weights.  One thread.
-__device__ inline void route_topk(const float *logit, int E, int K, int *idx, float *w) {
-    float m = logit[0];
-    for (int e = 1; e < E; ++e) m = fmaxf(m, logit[e]);
-    float p[kMaxExperts];
-    float z = 0.f;
-    for (int e = 0; e < E; ++e) {
-        p[e] = expf(logit[e] - m);
-        z += p[e];
+// The router's decision for one token (section 6.2: top-k gating over the
+// softmax of the router logits), by one wave: softmax over the E (<= 64)
+// logits, the top K (strictly larger wins, so the lower index wins exact
+// ties) and their weights renormalised over the K.  Lane e holds expert e;
+// every reduction is a register butterfly whose result is the same on all
+// lanes (max and arg-max are exact; the softmax sum is taken from lane 0),
+// and nothing is indexed at run time, so no private memory is used.  Lane
+// k < K ends with the expert of rank k in *idx and its weight in *w.
+__device__ inline void route_wave(const float *logit, int E, int K, int lane, int *idx, float *w) {
+    const bool in = lane < E;
+    const float l = in ? logit[lane] : -INFINITY;
+    float m = l;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    float p = in ? expf(l - m) : 0.f;
+    float z = p;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o, 64);
+    z = __shfl(z, 0, 64);
+    p *= 1.f / z;
+    bool taken = false;
+    float ps = 0.f, mine = 0.f;
+    int mi = -1;
+#pragma unroll
+    for (int k = 0; k < kMaxTopK; ++k) {
+        if (k < K) {
+            float v = (in && !taken) ? p : -1.f;  // probabilities are >= 0
+            int bi = lane;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) {
+                const float ov = __shfl_xor(v, o, 64);
+                const int oi = __shfl_xor(bi, o, 64);
+                if (ov > v || (ov == v && oi < bi)) {
+                    v = ov;
+                    bi = oi;
+                }
+            }
+            if (lane == bi) taken = true;
+            ps += v;
+            if (lane == k) {
+                mi = bi;
+                mine = v;
+            }
+        }
     }
-    const float inv = 1.f / z;
-    for (int e = 0; e < E; ++e) p[e] *= inv;
-    uint64_t taken = 0;
-    float ps = 0.f;
-    for (int k = 0; k < K; ++k) {
-        int best = -1;
-        for (int e = 0; e < E; ++e)
-            if (!((taken >> e) & 1ull) && (best < 0 || p[e] > p[best])) best = e;
-        taken |= 1ull << best;
-        idx[k] = best;
-        ps += p[best];
-    }
-    for (int k = 0; k < K; ++k) w[k] = p[idx[k]] / ps;
+    *idx = mi;
+    *w = mine / ps;
 }
 
 template <typename WT, int NC, bool DENSE, int RIF>
@@ -427,7 +450,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     if (a.route) {
         eoff = (size_t)a.route[slot] * a.expert_stride;
     } else if (a.wr) {
-        // the token's router: wave w dots expert rows w, w + 8, ...; thread 0
+        // the token's router: wave w dots expert rows w, w + 8, ...; wave 0
         // takes the softmax and top-k and picks this slot's expert
         const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.wr, (uint32_t)a.E * (uint32_t)H * (uint32_t)sizeof(WT));
         for (int e = wave; e < a.E; e += kWaves) {
@@ -450,15 +473,16 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
             if (lane == 0) s_logit[e] = d;
         }
         __syncthreads();
-        if (tid == 0) {
-            int idx[kMaxTopK];
-            float w[kMaxTopK];
-            route_topk(s_logit, a.E, a.K, idx, w);
-            const int k = slot % a.K;
-            s_expert = idx[k];
-            if (tile == 0) {
-                a.ridx[slot] = idx[k];
-                a.rw[slot] = w[k];
+        if (wave == 0) {
+            int ix;
+            float wv;
+            route_wave(s_logit, a.E, a.K, lane, &ix, &wv);
+            if (lane == slot % a.K) {
+                s_expert = ix;
+                if (tile == 0) {
+                    a.ridx[slot] = ix;
+                    a.rw[slot] = wv;
+                }
             }
         }
         __syncthreads();
@@ -1389,8 +1413,8 @@ __global__ __launch_bounds__(256) void ffn_union_count(const int32_t *__restrict
 
 // Router of the MoE layer, one 256-thread block per token: x in registers,
 // each wave dots two expert rows at a time (all loads in flight), then
-// thread 0 takes the softmax, the top-k (strictly larger wins, so the lower
-// index wins exact ties) and the renormalised weights.
+// wave 0 takes the softmax, the top-k and the renormalised weights
+// (route_wave).
 template <typename WT, int NC>
 __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, const WT *__restrict__ wr, int H,
                                                   int E, int K, int32_t *__restrict__ topk_idx,
@@ -1420,13 +1444,13 @@ __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, c
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int idx[kMaxTopK];
-        float w[kMaxTopK];
-        route_topk(s_l, E, K, idx, w);
-        for (int k = 0; k < K; ++k) {
-            topk_idx[(size_t)t * K + k] = idx[k];
-            topk_w[(size_t)t * K + k] = w[k];
+    if (wave == 0) {
+        int ix;
+        float wv;
+        route_wave(s_l, E, K, lane, &ix, &wv);
+        if (lane < K) {
+            topk_idx[(size_t)t * K + lane] = ix;
+            topk_w[(size_t)t * K + lane] = wv;
         }
     }
 }

@@ -202,8 +202,10 @@ bool plan_batch(int batch, int hidden, int inter, int experts, int top_k, ts_dty
     q.hpad = (hidden + kBxKQuant - 1) / kBxKQuant * kBxKQuant;
     q.ntiles = (inter + kBxRows - 1) / kBxRows;
     q.nslices = (hidden + kBxSliceCols - 1) / kBxSliceCols;
+    // down: about one workgroup per compute unit (measured: two rounds of
+    // workgroups, or two per unit, run slower than one with longer lists)
     int want = g_down_chunks.load();
-    if (want <= 0) want = std::max(1, 512 / (q.nslices * groups));
+    if (want <= 0) want = std::max(1, 256 / (q.nslices * groups));
     q.nchunks = std::max(1, std::min(want, q.ntiles));
     q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, kBxChunkTiles);
     q.nchunks = (q.ntiles + q.tpc - 1) / q.tpc;
