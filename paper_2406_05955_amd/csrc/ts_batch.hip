@@ -759,9 +759,10 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
 
 // out[t][:] = sum over routed ranks k (ascending) of w[t][k] times the sum
 // over chunks (ascending within each thread's share) of the partial row of
-// (group, slot) = tslot[t][k].  Block: 16 columns x 64 shares, fixed LDS tree.
+// (group, slot) = tslot[t][k].  Block: 16 columns x 64 shares, combined in a
+// fixed order (register butterflies inside each wave, one LDS step across).
 __global__ __launch_bounds__(256) void bx_reduce(BxArgs a) {
-    __shared__ f32x4 red[64][4];
+    __shared__ f32x4 red[4][4];
     const int t = blockIdx.y;
     const int q = threadIdx.x & 3;
     const int grp = threadIdx.x >> 2;
@@ -779,13 +780,20 @@ __global__ __launch_bounds__(256) void bx_reduce(BxArgs a) {
         acc.z = fmaf(w, v.z, acc.z);
         acc.w = fmaf(w, v.w, acc.w);
     }
-    red[grp][q] = acc;
-    __syncthreads();
-    for (int st = 32; st >= 1; st >>= 1) {
-        if (grp < st) red[grp][q] += red[grp + st][q];
-        __syncthreads();
+    // the 16 shares of a wave (lanes q + 4 j) by register butterflies, then
+    // the 4 waves through LDS; a fixed order either way
+#pragma unroll
+    for (int m = 4; m < 64; m <<= 1) {
+        acc.x += __shfl_xor(acc.x, m, 64);
+        acc.y += __shfl_xor(acc.y, m, 64);
+        acc.z += __shfl_xor(acc.z, m, 64);
+        acc.w += __shfl_xor(acc.w, m, 64);
     }
-    if (grp == 0 && c4 < nq) *reinterpret_cast<f32x4 *>(a.out + (size_t)t * a.H + c4 * 4) = red[0][q];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane < 4) red[wave][lane] = acc;
+    __syncthreads();
+    if (threadIdx.x < 4 && c4 < nq)
+        *reinterpret_cast<f32x4 *>(a.out + (size_t)t * a.H + c4 * 4) = (red[0][q] + red[1][q]) + (red[2][q] + red[3][q]);
 }
 
 // Activity report from the per-tile masks: one block per (token, rank).

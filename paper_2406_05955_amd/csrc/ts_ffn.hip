@@ -1279,7 +1279,8 @@ __global__ __launch_bounds__(kDownThreads) void ffn_down(DownArgs a) {
 // out[o][:] = sum over the slots s of output row o (ascending), of w_s times
 // the sum over rows r of partial[s][r][:]; w_s = 1 without routing.
 // Block: 16 columns (4 float4) x 64 row groups; a thread adds rows grp,
-// grp + 64, ... in order, the 64 shares are combined by a fixed LDS tree.
+// grp + 64, ... in order, and the 64 shares are combined in a fixed order
+// (register butterflies inside each wave, one LDS step across the waves).
 // Grid (column blocks, outputs): 256 workgroups for hidden 4096, so the
 // partial rows stream in one round trip.
 constexpr int kRedCols4 = 4;
@@ -1289,7 +1290,7 @@ constexpr int kRedUnroll = 4;
 __global__ __launch_bounds__(256) void ffn_reduce(const float *__restrict__ partial, int rows, int H,
                                                   int slots_per_out, const float *__restrict__ slot_w,
                                                   float *__restrict__ out) {
-    __shared__ f32x4 red[kRedGroups][kRedCols4];
+    __shared__ f32x4 red[4][kRedCols4];
     const int o = blockIdx.y;
     const int q = threadIdx.x % kRedCols4;
     const int grp = threadIdx.x / kRedCols4;
@@ -1317,13 +1318,20 @@ __global__ __launch_bounds__(256) void ffn_reduce(const float *__restrict__ part
             acc.w = fmaf(w, v[u].w, acc.w);
         }
     }
-    red[grp][q] = acc;
-    __syncthreads();
-    for (int st = kRedGroups / 2; st >= 1; st >>= 1) {
-        if (grp < st) red[grp][q] += red[grp + st][q];
-        __syncthreads();
+    // the 16 groups of a wave (lanes q + 4 j) by register butterflies, then
+    // the 4 waves through LDS; a fixed order either way
+#pragma unroll
+    for (int m = 4; m < 64; m <<= 1) {
+        acc.x += __shfl_xor(acc.x, m, 64);
+        acc.y += __shfl_xor(acc.y, m, 64);
+        acc.z += __shfl_xor(acc.z, m, 64);
+        acc.w += __shfl_xor(acc.w, m, 64);
     }
-    if (grp == 0 && c4 < nq) *reinterpret_cast<f32x4 *>(out + (size_t)o * H + c4 * 4) = red[0][q];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane < kRedCols4) red[wave][lane] = acc;
+    __syncthreads();
+    if (threadIdx.x < kRedCols4 && c4 < nq)
+        *reinterpret_cast<f32x4 *>(out + (size_t)o * H + c4 * 4) = (red[0][q] + red[1][q]) + (red[2][q] + red[3][q]);
 }
 
 // Activity report: per slot, concatenate the tiles' ascending segments into
