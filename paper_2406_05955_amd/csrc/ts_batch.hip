@@ -758,19 +758,22 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
 }
 
 // out[t][:] = sum over routed ranks k (ascending) of w[t][k] times the sum
-// over chunks (ascending within each thread's share) of the partial row of
-// (group, slot) = tslot[t][k].  Block: 16 columns x 64 shares, combined in a
-// fixed order (register butterflies inside each wave, one LDS step across).
+// over chunks of the partial row of (group, slot) = tslot[t][k].  Block:
+// 256 columns (64 float4, one per lane) x 4 share groups (one per wave); a
+// thread adds shares grp, grp + 4, ... (share k * nchunks + c) in order, and
+// the four groups' sums are combined in a fixed order through LDS.  One
+// block per (256 columns, token): the shares are few (top_k x chunks), so a
+// wide block keeps the grid small.
 __global__ __launch_bounds__(256) void bx_reduce(BxArgs a) {
-    __shared__ f32x4 red[4][4];
+    __shared__ f32x4 red[4][64];
     const int t = blockIdx.y;
-    const int q = threadIdx.x & 3;
-    const int grp = threadIdx.x >> 2;
-    const int c4 = blockIdx.x * 4 + q;
+    const int q = threadIdx.x & 63;
+    const int grp = threadIdx.x >> 6;
+    const int c4 = blockIdx.x * 64 + q;
     const int nq = a.H / 4;
     const int total = a.K * a.nchunks;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int p = grp; p < total; p += 64) {
+    for (int p = grp; p < total; p += 4) {
         const int k = p / a.nchunks, c = p % a.nchunks;
         const int g = a.tslot[(t * a.K + k) * 2], s = a.tslot[(t * a.K + k) * 2 + 1];
         const float w = a.topw ? a.topw[t * a.K + k] : 1.f;
@@ -780,19 +783,9 @@ __global__ __launch_bounds__(256) void bx_reduce(BxArgs a) {
         acc.z = fmaf(w, v.z, acc.z);
         acc.w = fmaf(w, v.w, acc.w);
     }
-    // the 16 shares of a wave (lanes q + 4 j) by register butterflies, then
-    // the 4 waves through LDS; a fixed order either way
-#pragma unroll
-    for (int m = 4; m < 64; m <<= 1) {
-        acc.x += __shfl_xor(acc.x, m, 64);
-        acc.y += __shfl_xor(acc.y, m, 64);
-        acc.z += __shfl_xor(acc.z, m, 64);
-        acc.w += __shfl_xor(acc.w, m, 64);
-    }
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    if (lane < 4) red[wave][lane] = acc;
+    red[grp][q] = acc;
     __syncthreads();
-    if (threadIdx.x < 4 && c4 < nq)
+    if (grp == 0 && c4 < nq)
         *reinterpret_cast<f32x4 *>(a.out + (size_t)t * a.H + c4 * 4) = (red[0][q] + red[1][q]) + (red[2][q] + red[3][q]);
 }
 
@@ -953,7 +946,7 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     case 32: launch_tok<32>(p, a, st); break;
     default: launch_tok<64>(p, a, st); break;
     }
-    launch("batch_reduce", bx_reduce, dim3((unsigned)((p.hidden / 4 + 3) / 4), (unsigned)p.batch), dim3(256), st, a);
+    launch("batch_reduce", bx_reduce, dim3((unsigned)((p.hidden / 4 + 63) / 64), (unsigned)p.batch), dim3(256), st, a);
     ts_status s = check_launch("batch path");
     if (s != TS_OK) return s;
     if (want_lists) {
