@@ -104,9 +104,13 @@ size_t ts_ffn_workspace_bytes(int batch, int hidden, int inter, ts_dtype wdtype)
  *   x [batch][hidden] fp32; w_gate, w_up, w_down_t [inter][hidden] wdtype;
  *   out [batch][hidden] fp32; stats nullable; ws/ws_bytes workspace;
  *   stream hipStream_t or NULL.
- * batch == 1 uses the fused single-token kernels; batch > 1 reads every
- * weight row at most once for the whole batch (rows of the union of the
- * tokens' active sets) and runs the contraction on the matrix cores.
+ * batch == 1 uses the pipelined single-token kernel.  batch > 1 with
+ * TS_BF16 weights reads every weight row at most once per pass of up to 64
+ * tokens (the rows of the union of the pass's active sets) and runs the
+ * contraction on the matrix cores, x and Combined entering as high + low
+ * bf16 parts (fp32-level accuracy); TS_F32 weights run the single-token
+ * kernels per token, and so does a TS_BF16 batch above 64 whose report asks
+ * for the union counts (they need a single pass).
  */
 ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
                         ts_dtype wdtype, int batch, int hidden, int inter, float *out,
@@ -208,7 +212,12 @@ size_t ts_moe_workspace_bytes(int batch, int hidden, int inter, int n_experts, i
  *   topk_w [batch][top_k] fp32 (nullable): their renormalised weights;
  *   stats (nullable): per (token, slot) report, see ts_ffn_stats;
  *   ws / ws_bytes / stream as above.
- * The routing decision never leaves the device.
+ * The routing decision never leaves the device.  Batch 1 (and TS_F32
+ * weights) run the pipelined single-token kernel, each workgroup computing
+ * its token's router; 2 <= batch <= 64 with TS_BF16 weights run the
+ * matrix-core path, each expert's tokens in groups of about twice the
+ * expected load (an expert drawing more takes further groups and reads its
+ * weights once more per group).
  */
 ts_status ts_moe_sparse(const float *x, const void *w_router, const void *w_gate, const void *w_up,
                         const void *w_down_t, ts_dtype wdtype, int batch, int hidden, int inter,
@@ -239,8 +248,10 @@ const char *ts_version(void);
  * Per-kernel timing.  While enabled, every ts_* call records a HIP event
  * pair around each kernel it launches, on the call's stream.  ts_prof_read
  * synchronises on the recorded events and returns, for the kernel named
- * `kernel` ("ffn_main", "ffn_reduce", "ffn_stats", "moe_router",
- * "batch_gate", "batch_up", "batch_down", "batch_reduce", "probe_read",
+ * `kernel` ("ffn_main", "ffn_reduce", "ffn_gate_up", "ffn_down",
+ * "ffn_topk_select", "ffn_given", "given_counts", "ffn_stats", "ffn_union",
+ * "moe_router", "batch_prep", "batch_gate_up", "batch_down",
+ * "batch_reduce", "batch_stats", "batch_union", "probe_read",
  * "probe_copy"), the number of launches and their summed duration in
  * milliseconds since the last ts_prof_reset.  Returns TS_ERR_HIP on a
  * HIP failure, TS_ERR_NULL for a NULL output pointer.  Not thread-safe.
