@@ -54,6 +54,8 @@ def parse_args():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--probe", action="store_true", help="also run the HBM read / copy probes")
     ap.add_argument("--tile", type=int, default=0, help="ffn_tile tuning knob (0 = default)")
+    ap.add_argument("--batch-sizes", default="8,32", help="batch workload: batch sizes")
+    ap.add_argument("--variants", default="independent,hot_cold", help="batch workload: token generators")
     return ap.parse_args()
 
 
@@ -513,22 +515,28 @@ def run_batch_workload(args, ts, synth, torch):
     import numpy as np
     out = []
     H, I, L = H_MISTRAL, I_MISTRAL, args.layers
-    for B in (8, 32):
-        for variant in ("independent", "hot_cold"):
+    for B in (int(b) for b in args.batch_sizes.split(",")):
+        for variant in args.variants.split(","):
             bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(I, seed=11)
             stack = Stack(ts, synth, L, B, H, I, gate_bias=bias, seed=2)
             counts = stack.counts()  # unions over the batch
             t_s = timed(torch, stack.step_sparse, args.steps, args.warmup)
-            t_d = timed(torch, stack.step_dense, args.steps, args.warmup)
+            t_d = None if args.no_dense else timed(torch, stack.step_dense, args.steps, args.warmup)
             alg = sum(2 * H * (I + ng + na) + 8 * B * H for ng, na in counts) / L
+            # per kernel: gate+up reads W_gate whole and the union's W_up rows, down the union's W_down_t rows
+            alg_gu = sum(2 * H * (I + ng) for ng, _ in counts) / L
+            alg_dn = sum(2 * H * na for _, na in counts) / L
             dense = 3 * 2 * H * I + 8 * B * H
             kt = batch_kernels(ts, torch, stack.step_sparse, max(3, args.steps // 3))
             out.append({"workload": f"mistral7b_ffn_stack_bf16_b{B}_{variant}", "batch": B, "layers": L,
                         "union_gate_fraction": sum(c[0] for c in counts) / (L * I),
                         "union_active_fraction": sum(c[1] for c in counts) / (L * I),
-                        "sparse_tokens_per_s_layer": B * L / t_s, "dense_tokens_per_s_layer": B * L / t_d,
-                        "speedup": t_d / t_s, "byte_bound_speedup": dense / alg,
-                        "sparse_GBps_touched": alg / (t_s / L) / 1e9, "dense_GBps": dense / (t_d / L) / 1e9,
+                        "sparse_tokens_per_s_layer": B * L / t_s,
+                        "dense_tokens_per_s_layer": B * L / t_d if t_d else None,
+                        "speedup": t_d / t_s if t_d else None, "byte_bound_speedup": dense / alg,
+                        "sparse_GBps_touched": alg / (t_s / L) / 1e9,
+                        "dense_GBps": dense / (t_d / L) / 1e9 if t_d else None,
+                        "gate_up_bytes_per_layer": alg_gu, "down_bytes_per_layer": alg_dn,
                         "us_per_layer": t_s / L * 1e6, **kt})
             del stack
             torch.cuda.empty_cache()
