@@ -179,3 +179,15 @@ def test_topk_checks():
     need = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
     assert call(wsb=need - 1) == WS
     assert call(B=0) == SHAPE
+
+
+def test_c_program_links_the_library_only():
+    """The plain-C ABI check links libturbosparse.so and the HIP runtime, and
+    nothing of Python or PyTorch."""
+    binp = os.path.join(ROOT, "tests", "c_abi", "_build", "c_smoke")
+    if not os.path.exists(binp):
+        pytest.skip("not built (__graft_entry__.build() builds it)")
+    deps = subprocess.run(["ldd", binp], capture_output=True, text=True).stdout
+    assert "libturbosparse.so" in deps and "not found" not in deps.split("libturbosparse.so")[1].split("\n")[0]
+    assert "amdhip64" in deps
+    assert "torch" not in deps and "python" not in deps
