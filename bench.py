@@ -480,7 +480,7 @@ def run_topk_workload(args, ts, synth, torch):
                     raise RuntimeError(f"ts_ffn_sparse_topk -> {rc}")
         t = timed(torch, step, args.steps, args.warmup)
         kt = {}
-        for k in ("ffn_gate_up", "ffn_topk_select", "ffn_down", "ffn_reduce"):
+        for k in ("ffn_gate_up", "ffn_topk_select", "ffn_down", "ffn_topk_down", "ffn_reduce"):
             n, ms = kernel_avg_ms(ts, torch, step, max(3, args.steps // 3), k)
             if n:
                 kt[k + "_us"] = ms * 1e3

@@ -126,7 +126,9 @@ ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, co
  * kept neurons only.  The activity report's A_t is the kept set (its
  * non-zero members).  keep >= 0 (TS_ERR_SHAPE otherwise); inter <= 16384
  * (TS_ERR_UNSUPPORTED otherwise: the per-token selection runs in on-chip
- * memory).  Other arguments as ts_ffn_sparse, same workspace size.
+ * memory).  Other arguments as ts_ffn_sparse, same workspace size.  A call
+ * without a report and one with it run different kernel sequences and give
+ * the same bits.
  */
 ts_status ts_ffn_sparse_topk(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
                              ts_dtype wdtype, int batch, int hidden, int inter, int keep, float *out,
@@ -249,7 +251,7 @@ const char *ts_version(void);
  * pair around each kernel it launches, on the call's stream.  ts_prof_read
  * synchronises on the recorded events and returns, for the kernel named
  * `kernel` ("ffn_main", "ffn_reduce", "ffn_gate_up", "ffn_down",
- * "ffn_topk_select", "ffn_given", "given_counts", "ffn_stats", "ffn_union",
+ * "ffn_topk_select", "ffn_topk_down", "ffn_given", "given_counts", "ffn_stats", "ffn_union",
  * "moe_router", "batch_prep", "batch_gate_up", "batch_down",
  * "batch_reduce", "batch_stats", "batch_union", "probe_read",
  * "probe_copy"), the number of launches and their summed duration in

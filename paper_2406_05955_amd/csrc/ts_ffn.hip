@@ -979,8 +979,10 @@ struct SelArgs {
     float *khseg;
 };
 
-// Exclusive prefix over the workgroup of one int per thread; returns it, and
-// the total in *sum.  s_w: kSelWaves ints of scratch.  Contains barriers.
+// Exclusive prefix over the workgroup (NW waves) of one int per thread;
+// returns it, and the total in *sum.  s_w: NW ints of scratch.  Contains
+// barriers.
+template <int NW = kSelWaves>
 __device__ __forceinline__ int sel_block_scan(int v, int *s_w, int *sum) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int inc = v;
@@ -993,7 +995,7 @@ __device__ __forceinline__ int sel_block_scan(int v, int *s_w, int *sum) {
     __syncthreads();
     int before = 0, all = 0;
 #pragma unroll
-    for (int w = 0; w < kSelWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
         const int t = s_w[w];
         before += w < wave ? t : 0;
         all += t;
@@ -1263,6 +1265,242 @@ __global__ __launch_bounds__(kDownThreads) void ffn_down(DownArgs a) {
     }
 
     // 3. waves -> the chunk's partial row slice (wave order fixed)
+#pragma unroll
+    for (int e = 0; e < CE; ++e) s_red[wave][lane * CE + e] = acc[e];
+    __syncthreads();
+    float *prow = a.partial + ((size_t)slot * a.nchunks + chunk) * H;
+    for (int i = tid; i < SW; i += kDownThreads) {
+        const int col = slice * SW + i;
+        float v = s_red[0][i];
+#pragma unroll
+        for (int w = 1; w < kDownWaves; ++w) v += s_red[w][i];
+        if (col < H) prow[col] = v;
+    }
+}
+
+// Top-k mask without a separate selection launch: every down workgroup of
+// a slot finds the slot's threshold itself (the same keys and the same
+// radix steps as ffn_topk_select, so all of them agree) and then runs
+// ffn_down's work over the kept rows of its chunk.  The slot's Combined
+// values (the padded per-tile lists of the emit-mode pipelined kernel) come
+// into LDS with buffer-to-LDS loads in one batch, next to the tiles' counts
+// and the chunk's neuron indices; each thread takes whole tiles, so a radix
+// pass touches only the listed entries.  The kept list of the chunk is
+// built tile after tile in ascending order, as ffn_down builds it from the
+// selection's lists, so both sequences give the same bits.
+struct TopkDownArgs {
+    DownArgs d;   // cnt / aseg / hseg: the emit-mode lists (tile = the pipelined kernel's tile)
+    int keep;
+};
+
+constexpr int kTdKeys = 65 * 256;  // LDS words for one slot's padded values (65 KB >= kSelSpan entries)
+
+template <typename WT>
+__global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
+    constexpr int CE = WTraits<WT>::CE;
+    constexpr int SW = 64 * CE;  // columns per slice
+    constexpr int TPT = kSelMaxTiles / kDownThreads;  // tiles per thread (selection)
+    constexpr int EPT = kDownMaxRows / kDownThreads;  // chunk positions per thread
+    const DownArgs &a = ta.d;
+
+    __shared__ __attribute__((aligned(16))) uint32_t s_key[kTdKeys];
+    __shared__ int s_tc[kSelMaxTiles];
+    __shared__ int s_ai[kDownMaxRows];
+    __shared__ int s_row[kDownMaxRows];
+    __shared__ float s_hv[kDownMaxRows];
+    __shared__ int s_cnt[kDownMaxTiles];
+    __shared__ int s_toff[kDownMaxTiles + 1];
+    __shared__ float s_red[kDownWaves][SW];
+    __shared__ uint32_t s_hist[256];
+    __shared__ int s_w[kDownWaves];
+    __shared__ uint32_t s_st[3];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int slice = blockIdx.x % a.nslices;
+    const int chunk = (blockIdx.x / a.nslices) % a.nchunks;
+    const int slot = blockIdx.x / (a.nslices * a.nchunks);
+    const int H = a.H;
+    const int nch = H / CE;
+    const int t0 = chunk * a.tpc;
+    const int ntc = min(a.tpc, a.ntiles - t0);
+    const size_t pr0 = (size_t)slot * a.ntiles;
+    const int span = a.ntiles * a.tile;
+    // a tile's entries are read four at a time (tiles are multiples of 4
+    // neurons, so every tile starts on a 16-byte boundary of s_key)
+    const u32x4 *s_key4 = reinterpret_cast<const u32x4 *>(s_key);
+    auto for_entries = [&](int t, auto &&f) {
+        const int c = s_tc[t], b4 = t * a.tile / 4;
+        for (int q0 = 0; q0 < c; q0 += 4) {
+            const u32x4 v = s_key4[b4 + q0 / 4];
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (q0 + i < c) f(q0 + i, w[i]);
+        }
+    };
+
+    // 0. one batch of loads: the slot's values into LDS, the tiles' counts,
+    //    the chunk's neuron indices
+    {
+        const uint32_t bytes = (uint32_t)span * 4u;
+        const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.hseg + pr0 * a.tile, bytes);
+        const int nkb = (int)((bytes + 1023u) / 1024u);  // 1 KB pieces, <= 65
+        for (int kb = wave; kb < nkb; kb += kDownWaves)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rh, s_key + kb * 256, 16, (uint32_t)kb * 1024u + lane * 16u, 0,
+                                                     0, 0);
+        int na[TPT];
+#pragma unroll
+        for (int j = 0; j < TPT; ++j) {
+            const int t = tid + kDownThreads * j;
+            na[j] = t < a.ntiles ? a.cnt[(pr0 + t) * 2 + 1] : 0;
+        }
+        int ai[EPT];
+        const size_t cb = (pr0 + t0) * a.tile;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int e = tid + kDownThreads * u;
+            ai[u] = e < ntc * a.tile ? a.aseg[cb + e] : 0;
+        }
+        for (int i = tid; i < 256; i += kDownThreads) s_hist[i] = 0u;
+        if (tid < 3) s_st[tid] = 0u;
+#pragma unroll
+        for (int j = 0; j < TPT; ++j) {
+            const int t = tid + kDownThreads * j;
+            if (t < a.ntiles) s_tc[t] = na[j];
+        }
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int e = tid + kDownThreads * u;
+            if (e < ntc * a.tile) s_ai[e] = ai[u];
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's pieces of the values are in LDS
+    }
+    __syncthreads();
+
+    // 1. k = min(keep, listed entries); the k-th largest key (fp32 bits of a
+    //    non-negative value order like the value)
+    int mine = 0;
+    for (int t = tid; t < a.ntiles; t += kDownThreads) mine += s_tc[t];
+    int n;
+    sel_block_scan<kDownWaves>(mine, s_w, &n);
+    const int k = min(ta.keep, n);
+    uint32_t thr = 0xffffffffu;  // no key reaches it: nothing kept (k = 0)
+    int tie_pos = -1;            // last kept position among keys equal to thr
+    if (k > 0) {
+        uint32_t mask = 0u;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            const uint32_t prefix = s_st[0];
+            for (int t = tid; t < a.ntiles; t += kDownThreads)
+                for_entries(t, [&](int, uint32_t v) {
+                    if ((v & mask) == prefix) atomicAdd(&s_hist[(v >> shift) & 255u], 1u);
+                });
+            __syncthreads();
+            if (wave == 0) sel_find_bin(s_hist, s_st, shift == 24 ? (uint32_t)k : s_st[1], shift, lane);
+            mask |= 255u << shift;
+            __syncthreads();
+        }
+        thr = s_st[0];
+        const uint32_t ties = s_st[1], neq = s_st[2];
+        tie_pos = 0x7fffffff;
+        if (ties < neq) {
+            // the ties-th smallest position among keys equal to thr (the
+            // ties-th largest of 0xffff - position)
+            __syncthreads();
+            if (tid == 0) s_st[0] = 0u;
+            __syncthreads();
+            mask = 0u;
+            for (int shift = 8; shift >= 0; shift -= 8) {
+                const uint32_t prefix = s_st[0];
+                for (int t = tid; t < a.ntiles; t += kDownThreads)
+                    for_entries(t, [&](int q, uint32_t v) {
+                        const uint32_t key = 0xffffu - (uint32_t)(t * a.tile + q);
+                        if (v == thr && (key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1u);
+                    });
+                __syncthreads();
+                if (wave == 0) sel_find_bin(s_hist, s_st, shift == 8 ? ties : s_st[1], shift, lane);
+                mask |= 255u << shift;
+                __syncthreads();
+            }
+            tie_pos = (int)(0xffffu - s_st[0]);
+        }
+    }
+
+    // 2. the chunk's kept rows, tile after tile, ascending
+    if (tid < ntc) {
+        const int t = t0 + tid;
+        int m = 0;
+        for_entries(t, [&](int q, uint32_t v) {
+            m += (v > thr || (v == thr && t * a.tile + q <= tie_pos)) ? 1 : 0;
+        });
+        s_cnt[tid] = m;
+    }
+    __syncthreads();
+    if (wave == 0) {  // offsets of the chunk's tiles (ntc <= 256: four per lane)
+        int c4[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = 4 * lane + i;
+            c4[i] = j < ntc ? s_cnt[j] : 0;
+            sum += c4[i];
+        }
+        int inc = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_up(inc, o, 64);
+            if (lane >= o) inc += t;
+        }
+        int off = inc - sum;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = 4 * lane + i;
+            if (j < ntc) s_toff[j] = off;
+            off += c4[i];
+        }
+        if (lane == 63) s_toff[ntc] = inc;  // the chunk's total
+    }
+    __syncthreads();
+    if (tid < ntc) {
+        const int t = t0 + tid;
+        int m = s_toff[tid];
+        for_entries(t, [&](int q, uint32_t v) {
+            if (v > thr || (v == thr && t * a.tile + q <= tie_pos)) {
+                s_row[m] = s_ai[tid * a.tile + q];
+                s_hv[m] = __uint_as_float(v);
+                ++m;
+            }
+        });
+    }
+    __syncthreads();
+    const int nrows = s_toff[ntc];
+
+    // 3. axpy over the rows (as ffn_down)
+    const WT *wd = reinterpret_cast<const WT *>(a.wd);
+    const int c = slice * 64 + lane;
+    float acc[CE];
+#pragma unroll
+    for (int e = 0; e < CE; ++e) acc[e] = 0.f;
+    for (int j0 = wave; j0 < nrows; j0 += kDownUnroll * kDownWaves) {
+        u32x4 v[kDownUnroll];
+        float hv[kDownUnroll];
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            const int j = j0 + u * kDownWaves;
+            const bool ok = j < nrows;
+            v[u] = ld_stream_masked(wd + (size_t)s_row[ok ? j : j0] * H, c, nch, 16, ok);
+            hv[u] = ok ? s_hv[j] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kDownUnroll; ++u) {
+            float f[CE];
+            unpack<WT>(v[u], f);
+#pragma unroll
+            for (int e = 0; e < CE; ++e) acc[e] = fmaf(hv[u], f[e], acc[e]);
+        }
+    }
+
+    // 4. waves -> the chunk's partial row slice (wave order fixed)
 #pragma unroll
     for (int e = 0; e < CE; ++e) s_red[wave][lane * CE + e] = acc[e];
     __syncthreads();
@@ -1776,6 +2014,30 @@ ts_status run_topk(const float *x, const void *wg, const void *wu, const void *w
     else launch_pipe<uint16_t, true>(p.nc, p.tile, grid, st, a);
     ts_status s = check_launch("ffn_gate_up");
     if (s != TS_OK) return s;
+    if (!stats) {
+        // no report: the down workgroups select for themselves
+        TopkDownArgs td;
+        td.d.wd = wd;
+        td.d.route = nullptr;
+        td.d.expert_stride = 0;
+        td.d.H = p.hidden;
+        td.d.tile = p.tile;
+        td.d.ntiles = p.ntiles;
+        td.d.nslices = p.nslices;
+        td.d.nchunks = p.pnchunks;
+        td.d.tpc = p.ptpc;
+        td.d.cnt = a.cnt;
+        td.d.aseg = a.aseg;
+        td.d.hseg = a.hseg;
+        td.d.partial = a.partial;
+        td.keep = keep;
+        const dim3 dg((unsigned)(p.slots * p.pnchunks * p.nslices));
+        if (dt == TS_F32) launch("ffn_topk_down", ffn_topk_down<float>, dg, dim3(kDownThreads), st, td);
+        else launch("ffn_topk_down", ffn_topk_down<uint16_t>, dg, dim3(kDownThreads), st, td);
+        s = check_launch("ffn_topk_down");
+        if (s != TS_OK) return s;
+        return launch_reduce(a.partial, p.pnchunks, p, nullptr, out, st);
+    }
     s = launch_select(p, p.ntiles, p.tile, keep, a.cnt, a.aseg, a.hseg, ws, st);
     if (s != TS_OK) return s;
     DownArgs d;

@@ -7,7 +7,9 @@ values have a clear gap between the keep-th and the next (relative 1e-4,
 some hundred times the fp32 accumulation error of a projection): there both
 sides keep the same neurons, and
 the reported active set must equal the oracle's kept set exactly.  Outputs:
-relative L2 <= 1e-5 with fp32 weights, <= 1e-2 with bf16 weights."""
+relative L2 <= 1e-5 with fp32 weights, <= 1e-2 with bf16 weights.  A call
+without the report takes the other kernel sequence (the down workgroups
+select for themselves); it must give the same bits as the call with it."""
 import numpy as np
 import pytest
 import torch
@@ -57,7 +59,9 @@ def check(inp, frac):
     y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype, keep)
     x, wg, wu, wd = ffn_inputs_to_dev(inp)
     out, st = ts.ffn_sparse_topk(x, wg, wu, wd, keep, stats=True)
+    fast = ts.ffn_sparse_topk(x, wg, wu, wd, keep)  # no report: the down workgroups select for themselves
     torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), fast.view(torch.int32))
     err = rel_l2(out.cpu().numpy(), y)
     assert err <= (1e-5 if inp.dtype == synth.F32 else 1e-2), (B, H, I, keep, err)
     thr = 1e-6 if inp.dtype == synth.F32 else 1e-4
@@ -103,12 +107,15 @@ def test_topk_keep_all_and_zero():
     x, wg, wu, wd = ffn_inputs_to_dev(inp)
     for keep in (2000, 5000, int(ref.n_active.max())):
         out, st = ts.ffn_sparse_topk(x, wg, wu, wd, keep, stats=True)
+        fast = ts.ffn_sparse_topk(x, wg, wu, wd, keep)
         torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int32), fast.view(torch.int32))
         assert rel_l2(out.cpu().numpy(), ref.y) <= 1e-5
         assert np.array_equal(st["n_active"].cpu().numpy(), ref.n_active)
     out, st = ts.ffn_sparse_topk(x, wg, wu, wd, 0, stats=True)
+    fast = ts.ffn_sparse_topk(x, wg, wu, wd, 0)
     torch.cuda.synchronize()
-    assert not out.any().item()
+    assert not out.any().item() and not fast.any().item()
     assert not st["n_active"].any().item()
     assert np.array_equal(st["n_gate"].cpu().numpy(), ref.n_gate)
 
@@ -138,7 +145,9 @@ def test_topk_ties_take_lower_index():
         keep = above + take
         y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype, keep)
         out, st = ts.ffn_sparse_topk(x, wg, wu, wd, keep, stats=True)
+        fast = ts.ffn_sparse_topk(x, wg, wu, wd, keep)
         torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int32), fast.view(torch.int32)), take
         got = set(list_of(st, "active_idx", 0, "n_active").tolist())
         assert set(trio[:take]) <= got and not (set(trio[take:]) & got), (take, trio)
         assert rel_l2(out.cpu().numpy(), y) <= 1e-2
@@ -178,7 +187,9 @@ def test_topk_token_with_no_open_gate():
     y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype, keep)
     x, wg, wu, wd = ffn_inputs_to_dev(inp)
     out, st = ts.ffn_sparse_topk(x, wg, wu, wd, keep, stats=True)
+    fast = ts.ffn_sparse_topk(x, wg, wu, wd, keep)
     torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), fast.view(torch.int32))
     o = out.cpu().numpy()
     assert not o[1].any()
     assert int(st["n_gate"][1]) == 0 and int(st["n_active"][1]) == 0
@@ -197,7 +208,9 @@ def test_topk_mistral_batch64():
     y, nk = oracle.ffn_topk(inp.x, inp.w_gate, inp.w_up, inp.w_down_t, inp.dtype, keep)
     x, wg, wu, wd = ffn_inputs_to_dev(inp)
     out, st = ts.ffn_sparse_topk(x, wg, wu, wd, keep, stats=True)
+    fast = ts.ffn_sparse_topk(x, wg, wu, wd, keep)
     torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), fast.view(torch.int32))
     o = out.cpu().numpy()
     checked = 0
     for t in range(64):
