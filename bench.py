@@ -54,6 +54,7 @@ def parse_args():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--probe", action="store_true", help="also run the HBM read / copy probes")
     ap.add_argument("--tile", type=int, default=0, help="ffn_tile tuning knob (0 = default)")
+    ap.add_argument("--tune", default="", help="further tuning knobs, KEY=VALUE[,KEY=VALUE...] (ts_tune_set)")
     ap.add_argument("--batch-sizes", default="8,32", help="batch workload: batch sizes")
     ap.add_argument("--variants", default="independent,hot_cold", help="batch workload: token generators")
     return ap.parse_args()
@@ -658,6 +659,9 @@ def main():
     from paper_2406_05955_amd import synth
     if args.tile:
         ts.tune_set("ffn_tile", args.tile)
+    for kv in filter(None, args.tune.split(",")):
+        k, v = kv.split("=")
+        ts.tune_set(k.strip(), int(v))
     if args.workload == "mistral":
         print(json.dumps(run_mistral(args, ts, synth, torch)), flush=True)
         return
