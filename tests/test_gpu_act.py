@@ -46,6 +46,7 @@ def check(inp, tau):
     (3, 520, 999, synth.BF16, 0.1),     # ragged, several tokens (per-token kernels)
     (2, 4096, 2048, synth.F32, 0.0),    # fp32 rows of 1024 chunks: the fused kernel
     (4, 2048, 3000, synth.BF16, 0.3),
+    (256, 128, 300, synth.BF16, 0.1),   # the largest batch
 ])
 def test_act_shapes(B, H, I, dtype, tau):
     inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[61, B, H, I])

@@ -47,7 +47,8 @@ def check_batch(inp, ref=None, union=True):
 
 @pytest.mark.parametrize("B,H,I", [(2, 512, 1000), (3, 200, 130), (8, 1024, 2048), (16, 64, 33), (17, 512, 700),
                                    (32, 1000, 1500), (33, 256, 512), (64, 512, 1024), (65, 256, 300),
-                                   (130, 128, 96), (5, 8, 1), (4, 4096, 3001)])
+                                   (130, 128, 96), (5, 8, 1), (4, 4096, 3001),
+                                   (256, 128, 96), (2, 8192, 300)])  # largest batch, widest rows
 def test_batch_shapes(B, H, I):
     inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=synth.BF16, seed=[31, B, H, I])
     check_batch(inp)

@@ -62,7 +62,8 @@ def test_config0_fp32_full():
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 @pytest.mark.parametrize("B,H,I", [(1, 8, 1), (1, 8, 7), (1, 40, 65), (3, 200, 130), (1, 1000, 777),
-                                   (2, 512, 4096), (1, 2048, 3001), (1, 4096, 2000)])
+                                   (2, 512, 4096), (1, 2048, 3001), (1, 4096, 2000),
+                                   (256, 64, 40)])  # the largest batch
 def test_ragged_shapes(dtype, B, H, I):
     if dtype == synth.BF16 and H % 8:
         H += 8 - H % 8

@@ -66,12 +66,13 @@ def check(inp, idx, count, stats=True):
     (2, 4096, 2048, synth.BF16, 1000),
     (5, 256, 300, synth.F32, 7),          # lists shorter than a chunk
     (2, 1024, 4000, synth.BF16, 4000),    # many chunks
+    (256, 128, 300, synth.F32, 50),       # the largest batch
 ])
 def test_given_random_lists(B, H, I, dtype, maxc):
     rng = np.random.default_rng(100 + B + H)
     inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[41, B, H, I])
     idx = random_lists(rng, B, I, maxc)
-    count = np.array([maxc - 3 * t for t in range(B)], np.int32)
+    count = np.array([maxc - (3 * t if B < 64 else t % maxc) for t in range(B)], np.int32)
     count[-1] = maxc + 50  # clamped to max_count
     check(inp, idx, count)
 

@@ -81,6 +81,7 @@ def check(inp, frac):
     (3, 520, 999, synth.BF16, 0.5),     # ragged, several tokens
     (2, 4096, 2048, synth.F32, 0.3),    # fp32 rows of 1024 chunks
     (4, 2048, 3000, synth.BF16, 0.7),
+    (256, 128, 200, synth.BF16, 0.5),   # the largest batch
 ])
 def test_topk_shapes(B, H, I, dtype, frac):
     inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[71, B, H, I])
