@@ -295,6 +295,11 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *                about twice the expected expert load; an expert with more
  *                tokens takes further groups), 1 = one group per expert
  *                with slots for the whole batch
+ *   "ffn_interleave" single-token kernels: 0 default (workgroup t takes
+ *                neurons t, t + T, t + 2 T, ... of T workgroups per token,
+ *                so the grid streams one narrow band of each matrix at a
+ *                time; used while a matrix is below 2 GB and inter <=
+ *                131072), 1 = contiguous tiles of neurons
  * Returns TS_ERR_SHAPE for an unknown key or out-of-range value.
  */
 ts_status ts_tune_set(const char *key, int value);

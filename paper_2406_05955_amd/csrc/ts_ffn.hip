@@ -119,6 +119,11 @@ struct SlotArgs {
     // `tau` (Combined = max(0, gate - tau) * up: ReGLU at tau = 0).
     int act;
     float tau;
+    // Neurons of a tile: rstride <= 1, tile t holds [t * tile, t * tile + tile);
+    // rstride = ntiles (interleaved), tile t holds t, t + ntiles, t + 2 ntiles,
+    // ..., so that at any moment the grid reads one narrow band of each
+    // matrix.  The segments hold neuron ids either way.
+    int rstride;
 };
 
 // The open-gate threshold and the Combined activation of a neuron whose
@@ -197,9 +202,11 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
     const int tile = blockIdx.x % a.ntiles;
     const int slot = blockIdx.x / a.ntiles;
     const int tok = slot / a.slots_per_tok;
-    const int n0 = tile * a.tile;
-    const int nt = min(a.tile, a.I - n0);
+    const int rs = a.rstride > 1 ? a.rstride : 1;
+    const int n0 = rs == 1 ? tile * a.tile : tile;
+    const int nt = rs == 1 ? min(a.tile, a.I - n0) : (a.I - n0 + rs - 1) / rs;
     const int H = a.H;
+    const size_t pitch = (size_t)H * rs;  // elements from one of the tile's rows to the next
     const int nch = H / CE;
 
     size_t eoff = 0;
@@ -218,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
 #pragma unroll
         for (int k = 0; k < RIF; ++k) {
             valid[k] = r + k * kWaves < nt;
-            rows[k] = wg + (size_t)(valid[k] ? r + k * kWaves : r) * H;
+            rows[k] = wg + (size_t)(valid[k] ? r + k * kWaves : r) * pitch;
         }
         float d[RIF];
         dot_rows<WT, NC, RIF>(rows, valid, xr, lane, nch, d);
@@ -250,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
         for (int k = 0; k < RIF; ++k) {
             valid[k] = q + k * kWaves < ng;
             li[k] = s_gl[valid[k] ? q + k * kWaves : q];
-            rows[k] = wu + (size_t)li[k] * H;
+            rows[k] = wu + (size_t)li[k] * pitch;
         }
         float u[RIF];
         dot_rows<WT, NC, RIF>(rows, valid, xr, lane, nch, u);
@@ -290,14 +297,15 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
 #pragma unroll
         for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
 
-    const __amdgpu_buffer_rsrc_t rd = make_rsrc(wd, (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT));
+    const __amdgpu_buffer_rsrc_t rd =
+        make_rsrc(wd, ((uint32_t)(nt - 1) * (uint32_t)rs + 1u) * (uint32_t)H * (uint32_t)sizeof(WT));
     for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
         u32x4 v[kDownUnroll][NCD];
 #pragma unroll
         for (int u = 0; u < kDownUnroll; ++u) {
             const int aa = a0 + u;
             const uint32_t base =
-                aa < na ? (uint32_t)s_al[aa] * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
+                aa < na ? (uint32_t)s_al[aa] * (uint32_t)pitch * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
             for (int kd = 0; kd < NCD; ++kd) {
                 const int c = tid + kThreads * kd;
@@ -335,8 +343,8 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
         a.cnt[pr * 2 + 1] = na;
     }
     if (a.want_seg) {
-        for (int q = tid; q < ng; q += kThreads) a.gseg[pr * a.tile + q] = n0 + s_gl[q];
-        for (int q = tid; q < na; q += kThreads) a.aseg[pr * a.tile + q] = n0 + s_al[q];
+        for (int q = tid; q < ng; q += kThreads) a.gseg[pr * a.tile + q] = n0 + s_gl[q] * rs;
+        for (int q = tid; q < na; q += kThreads) a.aseg[pr * a.tile + q] = n0 + s_al[q] * rs;
     }
 }
 
@@ -355,7 +363,7 @@ template <typename WT, int NC>
 struct PipeWave {
     static constexpr int CE = WTraits<WT>::CE;
     __amdgpu_buffer_rsrc_t rg, ru;  // the tile's W_gate / W_up rows
-    int H, nch, lane;
+    int pitch, nch, lane;  // pitch: elements from one of the tile's rows to the next
     int act;
     float tau;
     float (&xr)[NC][CE];
@@ -367,7 +375,7 @@ struct PipeWave {
     // separates a load from its consumer and all of a wave's loads stay in
     // flight across steps.
     __device__ void issue(__amdgpu_buffer_rsrc_t r, int row, u32x4 (&v)[NC]) {
-        const uint32_t base = row >= 0 ? (uint32_t)row * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
+        const uint32_t base = row >= 0 ? (uint32_t)row * (uint32_t)pitch * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
         for (int c0 = 0; c0 < NC; ++c0) {
             const int c = lane + 64 * c0;
@@ -436,8 +444,9 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     const int tile = blockIdx.x % a.ntiles;
     const int slot = blockIdx.x / a.ntiles;
     const int tok = slot / a.slots_per_tok;
-    const int n0 = tile * a.tile;
-    const int nt = min(a.tile, a.I - n0);
+    const int rs = a.rstride > 1 ? a.rstride : 1;
+    const int n0 = rs == 1 ? tile * a.tile : tile;
+    const int nt = rs == 1 ? min(a.tile, a.I - n0) : (a.I - n0 + rs - 1) / rs;
     const int H = a.H;
     const int nch = H / CE;
     const size_t pr = (size_t)slot * a.ntiles + tile;
@@ -491,9 +500,11 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     const WT *wg = reinterpret_cast<const WT *>(a.wg) + eoff + (size_t)n0 * H;
     const WT *wu = reinterpret_cast<const WT *>(a.wu) + eoff + (size_t)n0 * H;
     const WT *wd = reinterpret_cast<const WT *>(a.wd) + eoff + (size_t)n0 * H;
-    // buffer resources over the tile's rows (at most 128 rows of 32 KB)
-    const uint32_t tbytes = (uint32_t)nt * (uint32_t)H * (uint32_t)sizeof(WT);
-    PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H, nch, lane, a.act, a.tau, xr, s_g, s_h, s_on};
+    // buffer resources from the tile's first row to the end of its last
+    // (contiguous: at most 128 rows of 32 KB; interleaved: below 2 GB, which
+    // the host checks)
+    const uint32_t tbytes = ((uint32_t)(nt - 1) * (uint32_t)rs + 1u) * (uint32_t)H * (uint32_t)sizeof(WT);
+    PipeWave<WT, NC> pw{make_rsrc(wg, tbytes), make_rsrc(wu, tbytes), H * rs, nch, lane, a.act, a.tau, xr, s_g, s_h, s_on};
 
     // this wave's rows: wave, wave + 8, ...; first two gate rows in flight
     const int nrow = wave < nt ? (nt - wave + kWaves - 1) / kWaves : 0;
@@ -521,14 +532,14 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
             const bool in = r < nt;
             const bool pg = in && s_g[r] > gate_threshold(a.act, a.tau);
             const uint64_t mg = __ballot(pg);
-            if (pg && a.want_seg) a.gseg[pr * a.tile + ng + lane_prefix(mg, lane)] = n0 + r;
+            if (pg && a.want_seg) a.gseg[pr * a.tile + ng + lane_prefix(mg, lane)] = n0 + r * rs;
             const bool pa = in && s_on[r];
             const uint64_t ma = __ballot(pa);
             if (pa) {
                 const int pos = na0 + lane_prefix(ma, lane);
                 s_al[pos] = r;
                 s_av[pos] = s_h[r];
-                if (EMIT || a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r;
+                if (EMIT || a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r * rs;
                 if (EMIT) a.hseg[pr * a.tile + pos] = s_h[r];
             }
             ng += __popcll(mg);
@@ -563,7 +574,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
         for (int u = 0; u < kDownUnroll; ++u) {
             const int aa = a0 + u;
             const uint32_t base =
-                aa < na ? (uint32_t)s_al[aa] * (uint32_t)H * (uint32_t)sizeof(WT) : kOutOfRange;
+                aa < na ? (uint32_t)s_al[aa] * (uint32_t)(H * rs) * (uint32_t)sizeof(WT) : kOutOfRange;
 #pragma unroll
             for (int kd = 0; kd < NCD; ++kd) {
                 const int c = tid + kThreads * kd;
@@ -1619,6 +1630,66 @@ __global__ __launch_bounds__(256) void ffn_stats(const int32_t *__restrict__ cnt
     }
 }
 
+// Activity report for interleaved tiles (a tile's segment is ascending but
+// the tiles interleave): per slot, the members of G and A become bits of
+// two bitmaps in LDS (OR is order-free), then each thread turns a
+// contiguous run of words into ascending indices at its offset from a block
+// scan of the words' population counts.  One 256-thread block per slot.
+__global__ __launch_bounds__(256) void ffn_stats_ilv(const int32_t *__restrict__ cnt, const int32_t *__restrict__ gseg,
+                                                     const int32_t *__restrict__ aseg, int ntiles, int tile, int inter,
+                                                     int32_t *n_gate, int32_t *n_active, int32_t *gate_idx,
+                                                     int32_t *active_idx) {
+    __shared__ uint32_t s_bm[2][kIlvMaxInter / 32];
+    __shared__ int s_sc[2][256];
+    const int slot = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int nw = (inter + 31) / 32;
+    for (int i = tid; i < nw; i += 256) s_bm[0][i] = s_bm[1][i] = 0u;
+    __syncthreads();
+    for (int p = tid; p < ntiles; p += 256) {
+        const size_t pr = (size_t)slot * ntiles + p;
+        const int cg = cnt[pr * 2], ca = cnt[pr * 2 + 1];
+        for (int q = 0; q < cg; ++q) {
+            const int n = gseg[pr * tile + q];
+            atomicOr(&s_bm[0][n >> 5], 1u << (n & 31));
+        }
+        for (int q = 0; q < ca; ++q) {
+            const int n = aseg[pr * tile + q];
+            atomicOr(&s_bm[1][n >> 5], 1u << (n & 31));
+        }
+    }
+    __syncthreads();
+    const int per = (nw + 255) / 256;
+    const int w0 = min(nw, tid * per), w1 = min(nw, w0 + per);
+    int c[2] = {0, 0};
+    for (int w = w0; w < w1; ++w) {
+        c[0] += __popc(s_bm[0][w]);
+        c[1] += __popc(s_bm[1][w]);
+    }
+    s_sc[0][tid] = c[0];
+    s_sc[1][tid] = c[1];
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int v0 = tid >= off ? s_sc[0][tid - off] : 0;
+        const int v1 = tid >= off ? s_sc[1][tid - off] : 0;
+        __syncthreads();
+        s_sc[0][tid] += v0;
+        s_sc[1][tid] += v1;
+        __syncthreads();
+    }
+    int32_t *dst[2] = {gate_idx, active_idx};
+    for (int k = 0; k < 2; ++k) {
+        if (!dst[k]) continue;
+        int o = s_sc[k][tid] - c[k];
+        for (int w = w0; w < w1; ++w)
+            for (uint32_t b = s_bm[k][w]; b; b &= b - 1u) dst[k][(size_t)slot * inter + o++] = w * 32 + __ffs(b) - 1;
+    }
+    if (tid == 0) {
+        if (n_gate) n_gate[slot] = s_sc[0][255];
+        if (n_active) n_active[slot] = s_sc[1][255];
+    }
+}
+
 // Union of the slots' sets: flags[2][inter] set to 1 for members (plain
 // stores of the same value, so overlapping writers agree), then counted.
 __global__ void fill_i32(int32_t *p, size_t n, int32_t v) {
@@ -1820,12 +1891,13 @@ void launch_router(int nc, int batch, hipStream_t st, const float *x, const void
 }
 
 ts_status run_report(const SlotPlan &p, const int32_t *cnt, const int32_t *gseg, const int32_t *aseg, int ntiles,
-                     int tile, const ts_ffn_stats *stats, void *ws, hipStream_t st) {
+                     int tile, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool interleaved = false) {
     if (!stats) return TS_OK;
     if (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx) {
         ProfScope ps("ffn_stats", st);
-        hipLaunchKernelGGL(ffn_stats, dim3((unsigned)p.slots), dim3(256), 0, st, cnt, gseg, aseg, ntiles, tile,
-                           p.inter, stats->n_gate, stats->n_active, stats->gate_idx, stats->active_idx);
+        hipLaunchKernelGGL(interleaved ? ffn_stats_ilv : ffn_stats, dim3((unsigned)p.slots), dim3(256), 0, st, cnt,
+                           gseg, aseg, ntiles, tile, p.inter, stats->n_gate, stats->n_active, stats->gate_idx,
+                           stats->active_idx);
         ts_status s = check_launch("ffn_stats");
         if (s != TS_OK) return s;
     }
@@ -1963,6 +2035,12 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     a.aseg = ws_at<int32_t>(ws, p.off_aseg);
     a.partial = ws_at<float>(ws, p.off_partial);
     a.want_seg = want_seg ? 1 : 0;
+    // interleaved tiles (measured faster) where every row offset fits the
+    // 32-bit buffer offsets below kOutOfRange and the report's bitmaps fit
+    const bool ilv = tuned("ffn_interleave") == 0 && a.ntiles > 1 && p.inter <= kIlvMaxInter &&
+                     (unsigned long long)p.inter * (unsigned long long)p.hidden * (unsigned long long)p.esz <
+                         (unsigned long long)kOutOfRange;
+    a.rstride = ilv ? a.ntiles : 1;
     {
         dim3 grid((unsigned)(p.slots * a.ntiles));
         const int rif = rows_in_flight(p.nc);
@@ -1981,7 +2059,7 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     if (s != TS_OK) return s;
     s = launch_reduce(a.partial, a.ntiles, p, slot_w, out, st);
     if (s != TS_OK) return s;
-    return run_report(p, a.cnt, a.gseg, a.aseg, a.ntiles, a.tile, stats, ws, st);
+    return run_report(p, a.cnt, a.gseg, a.aseg, a.ntiles, a.tile, stats, ws, st, ilv);
 }
 
 // The kernel sequence run_slots picks: the pipelined kernel unless the dense

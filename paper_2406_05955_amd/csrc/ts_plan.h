@@ -28,6 +28,7 @@ constexpr int kDownMaxTiles = 256;        // gate+up tiles one down workgroup ca
 constexpr int kSelMax = 16384;            // Combined values the top-k selection holds in LDS (inter limit)
 constexpr int kSelMaxTiles = 2048;        // gate+up tiles per slot the selection lists (inter / 8)
 constexpr int kSelSpan = kSelMax + 128;   // padded list positions per slot it holds (last tile's padding)
+constexpr int kIlvMaxInter = 131072;     // interleaved tiles: the activity report's LDS bitmaps hold this many neurons
 
 // Workspace layout and launch shape shared by the single-token path (one
 // "slot" = one (token, expert) pair processed against one weight set).

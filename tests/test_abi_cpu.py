@@ -111,6 +111,9 @@ def test_tune_checks():
     assert ts.lib.ts_tune_set(b"ffn_tile", 132) == SHAPE
     assert ts.lib.ts_tune_set(b"nope", 8) == SHAPE
     assert ts.lib.ts_tune_set(b"ffn_tile", 32) == OK
+    assert ts.lib.ts_tune_set(b"ffn_interleave", 2) == SHAPE
+    assert ts.lib.ts_tune_set(b"ffn_interleave", 1) == OK
+    assert ts.lib.ts_tune_set(b"ffn_interleave", 0) == OK
     small = ts.ffn_workspace_bytes(1, 4096, 14336, 1)
     assert ts.lib.ts_tune_set(b"ffn_tile", 0) == OK
     assert ts.ffn_workspace_bytes(1, 4096, 14336, 1) < small

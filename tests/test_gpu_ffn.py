@@ -181,3 +181,30 @@ def test_kernel_variants(path, rif, gtile, chunks, dtype, B, H, I):
     finally:
         for k in ("ffn_path", "rif", "gate_tile", "down_chunks"):
             ts.tune_set(k, 0)
+
+
+@pytest.mark.parametrize("dtype,B,H,I", [(synth.BF16, 1, 4096, 14336), (synth.F32, 1, 512, 1792),
+                                         (synth.BF16, 1, 1000 + 8, 300), (synth.F32, 3, 1000, 3001),
+                                         (synth.F32, 2, 40, 65)])
+@pytest.mark.parametrize("path", [0, 2])
+def test_interleaved_tiles(dtype, B, H, I, path):
+    """Interleaved tiles (tile t holds neurons t, t + ntiles, ...; the default)
+    against contiguous ones: every neuron's gate and up are the same
+    computation either way, so the reported sets agree exactly; the outputs
+    differ only in how the down sums group into partial rows.  Both match
+    the oracle."""
+    inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=dtype, seed=[81, B, H, I, path])
+    ts.tune_set("ffn_path", path)
+    try:
+        out_i, st_i, ref = check_ffn(inp)
+        ts.tune_set("ffn_interleave", 1)
+        out_c, st_c, _ = check_ffn(inp, ref=ref)
+    finally:
+        ts.tune_set("ffn_interleave", 0)
+        ts.tune_set("ffn_path", 0)
+    for cnt, lst in (("n_gate", "gate_idx"), ("n_active", "active_idx")):
+        assert torch.equal(st_i[cnt], st_c[cnt]), cnt
+        for t in range(B):
+            n = int(st_i[cnt][t])
+            assert torch.equal(st_i[lst][t, :n], st_c[lst][t, :n]), (lst, t)
+    assert rel_l2(out_i.cpu().numpy(), out_c.cpu().numpy().astype(np.float64)) <= 1e-6
