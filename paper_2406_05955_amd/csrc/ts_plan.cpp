@@ -164,8 +164,6 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     off = align256(off + gst * (size_t)gt * sizeof(float));
     q.off_dpartial = off;
     off = align256(off + (size_t)slots * q.nchunks * (size_t)hidden * sizeof(float));
-    q.off_ctr = off;
-    off = align256(off + (size_t)q.outs * q.nslices * sizeof(int32_t));
     const size_t kst = std::max(gst, (size_t)slots * (size_t)q.ntiles);
     const size_t kseg = std::max(gst * (size_t)gt, (size_t)slots * (size_t)q.ntiles * q.tile);
     q.off_kcnt = off;

@@ -55,7 +55,7 @@ struct SlotPlan {
     // byte offsets into the workspace
     size_t off_cnt = 0, off_gseg = 0, off_aseg = 0, off_partial = 0;
     size_t off_route_idx = 0, off_route_w = 0, off_aux = 0;
-    size_t off_gcnt = 0, off_ggseg = 0, off_gaseg = 0, off_ghseg = 0, off_dpartial = 0, off_ctr = 0;
+    size_t off_gcnt = 0, off_ggseg = 0, off_gaseg = 0, off_ghseg = 0, off_dpartial = 0;
     size_t off_hseg = 0;  // Combined values of aseg (pipelined kernel's emit mode)
     // the top-k mask's kept lists (either kernel's tile layout)
     size_t off_kcnt = 0, off_kaseg = 0, off_khseg = 0;

@@ -60,12 +60,11 @@ int main() {
                             // workspace regions ordered, aligned and inside total
                             size_t offs[] = {p.off_cnt, p.off_gseg, p.off_aseg, p.off_partial, p.off_route_idx,
                                              p.off_route_w, p.off_aux, p.off_gcnt, p.off_ggseg, p.off_gaseg,
-                                             p.off_ghseg, p.off_dpartial, p.off_ctr, p.total};
+                                             p.off_ghseg, p.off_dpartial, p.off_kcnt, p.total};
                             for (int k = 1; k < 14; ++k)
                                 if (offs[k] < offs[k - 1] || offs[k] % 256) return fail("ws layout", 1, H, I, S);
                             size_t need_dp = (size_t)S * p.nchunks * H * 4;
-                            if (p.off_ctr - p.off_dpartial < need_dp) return fail("dpartial size", 1, H, I, S);
-                            if (p.total - p.off_ctr < (size_t)p.outs * p.nslices * 4) return fail("ctr size", 1, H, I, S);
+                            if (p.off_kcnt - p.off_dpartial < need_dp) return fail("dpartial size", 1, H, I, S);
                             if (p.off_gaseg - p.off_ggseg < (size_t)S * p.gntiles * p.gtile * 4)
                                 return fail("gseg size", 1, H, I, S);
                         }
