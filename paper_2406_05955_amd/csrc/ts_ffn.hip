@@ -962,8 +962,8 @@ __global__ __launch_bounds__(kGateThreads) void ffn_gate_up(GateArgs a) {
 // the value), ties to the lower neuron index, and rewrite each tile's active
 // list with the kept entries only, so the down kernel reads only their
 // W_down_t rows.  One 1024-thread workgroup per slot reads the padded
-// [ntiles][tile] lists (padding: index -1), whose positions run in
-// ascending neuron order:
+// [ntiles][tile] lists (padding: index -1; each tile's list ascending, the
+// tiles contiguous or interleaved):
 //   1. one batch of loads; the entries are compacted into LDS (one block
 //      scan) as key = (fp32 bits of the value) + 1 (order-preserving for
 //      non-negative floats, never 0), position and neuron index, and the
@@ -972,8 +972,9 @@ __global__ __launch_bounds__(kGateThreads) void ffn_gate_up(GateArgs a) {
 //      min(keep, entries) (histograms by LDS atomics: counts do not depend
 //      on order, so the result is deterministic; each bin search is one
 //      wave's suffix scan);
-//   3. when only some of the keys equal to the k-th are kept, the last kept
-//      position among them by a second radix select (over positions);
+//   3. when only some of the keys equal to the k-th are kept, the largest
+//      kept neuron index among them by a second radix select (over
+//      indices, so the tile layout does not matter);
 //   4. kept flags set in a bitmap by position; each kept entry's place in
 //      its tile's list is the number of kept positions before it in the
 //      tile; the tiles' kept counts likewise.
@@ -1124,7 +1125,7 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
 
     // 2. the k-th largest key
     uint32_t thr = 0xffffffffu;  // no key reaches it: nothing kept (k = 0)
-    uint32_t tie_pos = 0xffffu;  // last kept position among keys equal to thr
+    uint32_t tie_n = 0xffffu;  // largest kept neuron index among keys equal to thr
     if (k > 0) {
         uint32_t mask = 0u;
         for (int shift = 24; shift >= 0; shift -= 8) {
@@ -1143,7 +1144,8 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
         thr = s_st[0];
         const uint32_t ties = s_st[1], neq = s_st[2];
         // 3. only some of the keys equal to thr kept: the ties-th smallest
-        //    position among them (the ties-th largest of 0xffff - position)
+        //    neuron index among them (the ties-th largest of 0xffff - index;
+        //    indices < kSelMax)
         if (ties < neq) {
             __syncthreads();
             if (tid == 0) s_st[0] = 0u;
@@ -1152,7 +1154,7 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
             for (int shift = 8; shift >= 0; shift -= 8) {
                 const uint32_t prefix = s_st[0];
                 for (int i = tid; i < n; i += kSelThreads) {
-                    const uint32_t q = 0xffffu - s_cp[i];
+                    const uint32_t q = 0xffffu - s_ci[i];
                     if (s_c[i] == thr && (q & mask) == prefix) atomicAdd(&s_hist[(q >> shift) & 255u], 1u);
                 }
                 __syncthreads();
@@ -1160,14 +1162,14 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
                 mask |= 255u << shift;
                 __syncthreads();
             }
-            tie_pos = 0xffffu - s_st[0];
+            tie_n = 0xffffu - s_st[0];
         }
     }
 
     // 4. kept flags by position, then the compacted per-tile lists
     for (int i = tid; i < n; i += kSelThreads) {
         const uint32_t v = s_c[i], pos = s_cp[i];
-        if (v > thr || (v == thr && pos <= tie_pos)) atomicOr(&s_kb[pos >> 5], 1u << (pos & 31));
+        if (v > thr || (v == thr && s_ci[i] <= tie_n)) atomicOr(&s_kb[pos >> 5], 1u << (pos & 31));
     }
     __syncthreads();
     for (int i = tid; i < n; i += kSelThreads) {
@@ -1398,7 +1400,7 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
     sel_block_scan<kDownWaves>(mine, s_w, &n);
     const int k = min(ta.keep, n);
     uint32_t thr = 0xffffffffu;  // no key reaches it: nothing kept (k = 0)
-    int tie_pos = -1;            // last kept position among keys equal to thr
+    int tie_n = -1;              // largest kept neuron index among keys equal to thr
     if (k > 0) {
         uint32_t mask = 0u;
         for (int shift = 24; shift >= 0; shift -= 8) {
@@ -1414,10 +1416,11 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
         }
         thr = s_st[0];
         const uint32_t ties = s_st[1], neq = s_st[2];
-        tie_pos = 0x7fffffff;
+        tie_n = 0x7fffffff;
         if (ties < neq) {
-            // the ties-th smallest position among keys equal to thr (the
-            // ties-th largest of 0xffff - position)
+            // the ties-th smallest neuron index among keys equal to thr (the
+            // ties-th largest of 0xffff - index; indices < kSelMax); only
+            // the tied entries' indices are read, from the lists in memory
             __syncthreads();
             if (tid == 0) s_st[0] = 0u;
             __syncthreads();
@@ -1426,15 +1429,17 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
                 const uint32_t prefix = s_st[0];
                 for (int t = tid; t < a.ntiles; t += kDownThreads)
                     for_entries(t, [&](int q, uint32_t v) {
-                        const uint32_t key = 0xffffu - (uint32_t)(t * a.tile + q);
-                        if (v == thr && (key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1u);
+                        if (v == thr) {
+                            const uint32_t key = 0xffffu - (uint32_t)a.aseg[(pr0 + t) * a.tile + q];
+                            if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1u);
+                        }
                     });
                 __syncthreads();
                 if (wave == 0) sel_find_bin(s_hist, s_st, shift == 8 ? ties : s_st[1], shift, lane);
                 mask |= 255u << shift;
                 __syncthreads();
             }
-            tie_pos = (int)(0xffffu - s_st[0]);
+            tie_n = (int)(0xffffu - s_st[0]);
         }
     }
 
@@ -1443,7 +1448,7 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
         const int t = t0 + tid;
         int m = 0;
         for_entries(t, [&](int q, uint32_t v) {
-            m += (v > thr || (v == thr && t * a.tile + q <= tie_pos)) ? 1 : 0;
+            m += (v > thr || (v == thr && s_ai[tid * a.tile + q] <= tie_n)) ? 1 : 0;
         });
         s_cnt[tid] = m;
     }
@@ -1476,7 +1481,7 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
         const int t = t0 + tid;
         int m = s_toff[tid];
         for_entries(t, [&](int q, uint32_t v) {
-            if (v > thr || (v == thr && t * a.tile + q <= tie_pos)) {
+            if (v > thr || (v == thr && s_ai[tid * a.tile + q] <= tie_n)) {
                 s_row[m] = s_ai[tid * a.tile + q];
                 s_hv[m] = __uint_as_float(v);
                 ++m;
@@ -1890,6 +1895,15 @@ void launch_router(int nc, int batch, hipStream_t st, const float *x, const void
     }
 }
 
+// Interleaved tiles for the single-token kernels (measured faster) where
+// every row offset fits the 32-bit buffer offsets below kOutOfRange and the
+// report's bitmaps hold inter.
+bool interleave_tiles(const SlotPlan &p, int ntiles) {
+    return tuned("ffn_interleave") == 0 && ntiles > 1 && p.inter <= kIlvMaxInter &&
+           (unsigned long long)p.inter * (unsigned long long)p.hidden * (unsigned long long)p.esz <
+               (unsigned long long)kOutOfRange;
+}
+
 ts_status run_report(const SlotPlan &p, const int32_t *cnt, const int32_t *gseg, const int32_t *aseg, int ntiles,
                      int tile, const ts_ffn_stats *stats, void *ws, hipStream_t st, bool interleaved = false) {
     if (!stats) return TS_OK;
@@ -2035,11 +2049,7 @@ ts_status run_fused(const float *x, const void *wg, const void *wu, const void *
     a.aseg = ws_at<int32_t>(ws, p.off_aseg);
     a.partial = ws_at<float>(ws, p.off_partial);
     a.want_seg = want_seg ? 1 : 0;
-    // interleaved tiles (measured faster) where every row offset fits the
-    // 32-bit buffer offsets below kOutOfRange and the report's bitmaps fit
-    const bool ilv = tuned("ffn_interleave") == 0 && a.ntiles > 1 && p.inter <= kIlvMaxInter &&
-                     (unsigned long long)p.inter * (unsigned long long)p.hidden * (unsigned long long)p.esz <
-                         (unsigned long long)kOutOfRange;
+    const bool ilv = interleave_tiles(p, a.ntiles);
     a.rstride = ilv ? a.ntiles : 1;
     {
         dim3 grid((unsigned)(p.slots * a.ntiles));
@@ -2090,6 +2100,10 @@ ts_status run_topk(const float *x, const void *wg, const void *wu, const void *w
     a.hseg = ws_at<float>(ws, p.off_hseg);
     a.partial = ws_at<float>(ws, p.off_partial);
     a.want_seg = stats && (stats->gate_idx || stats->active_idx || stats->n_union) ? 1 : 0;
+    // (the selection breaks ties by neuron index, so the tile layout does
+    // not change which neurons are kept)
+    const bool ilv = interleave_tiles(p, p.ntiles);
+    a.rstride = ilv ? p.ntiles : 1;
     const dim3 grid((unsigned)(p.slots * p.ntiles));
     if (dt == TS_F32) launch_pipe<float, true>(p.nc, p.tile, grid, st, a);
     else launch_pipe<uint16_t, true>(p.nc, p.tile, grid, st, a);
@@ -2144,7 +2158,7 @@ ts_status run_topk(const float *x, const void *wg, const void *wu, const void *w
     if (s != TS_OK) return s;
     s = launch_reduce(d.partial, p.pnchunks, p, nullptr, out, st);
     if (s != TS_OK) return s;
-    return run_report(p, d.cnt, a.gseg, d.aseg, p.ntiles, p.tile, stats, ws, st);
+    return run_report(p, d.cnt, a.gseg, d.aseg, p.ntiles, p.tile, stats, ws, st, ilv);
 }
 
 
