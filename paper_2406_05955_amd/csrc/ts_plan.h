@@ -109,6 +109,7 @@ size_t given_ws_bytes(int batch, int hidden, int inter, int max_count, ts_dtype 
 
 int tuned_tile();
 int choose_tile(int inter, int slots, int cap);
+int choose_fused_tile(int inter, int slots);
 int tuned(const char *key);
 bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p);
 bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p);
