@@ -8,8 +8,13 @@
 // unchanged, so only the W_up rows of open gates and the W_down rows of
 // non-zero Combined activations are read.
 //
-// Two kernel sequences serve a call (both end in ffn_reduce, which sums
+// Three kernel sequences serve a call (all end in ffn_reduce, which sums
 // fp32 partial rows in a fixed order: deterministic, no atomics):
+//
+// pipe   (ffn_pipe, the default): as fused below, but each wave streams its
+//        gate rows two deep and issues an open row's W_up loads at once, so
+//        the up traffic travels with the gate stream (described at the
+//        kernel).
 //
 // fused  (ffn_fused, 8 waves per workgroup, one tile of neurons each)
 //   gate   every lane holds its share of x in registers; each wave dots whole
@@ -22,6 +27,9 @@
 //          an axpy over the W_down_t rows of A in ascending order into the
 //          tile's partial output row.
 //   The dense comparator is this kernel with every neuron taken.
+//   In pipe and fused the tiles interleave (tile t of T holds t, t + T, ...)
+//   where the matrices allow it, so the grid streams one narrow band of
+//   each matrix at a time.
 //
 // split  (ffn_gate_up with 4-wave workgroups, then ffn_down)
 //   gate and up as above, the tile's A segment and Combined values go to the
@@ -613,7 +621,7 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
 // ---------------------------------------------------------------------------
 // Given-list kernel (ts_ffn_sparse_given): per-wave gate / up stream and
 // down axpy as in the pipelined kernel, over a chunk of a token's neuron
-// list instead of a tile of consecutive neurons; a listed neuron's W_gate
+// list instead of a tile of neurons; a listed neuron's W_gate
 // and W_up rows are requested together.  The chunk's entries are staged
 // in LDS (entries outside [0, inter) become -1); each row load goes through
 // a buffer resource over that one row, an unused slot or a skipped entry
