@@ -50,7 +50,14 @@
 
 namespace ts {
 
-constexpr int kDownUnroll = 8;
+// W_down_t rows whose loads are in flight together in the down phases: 16
+// covers the active rows of all but ~0.1% of 56-neuron tiles at 90%
+// sparsity in one round trip (8 left ~9% of the tiles a second one, and the
+// slowest tile sets the kernel's end: 0.2 us per layer)
+constexpr int kDownUnroll = 16;
+// ffn_given builds a buffer resource per row; its short chunks (often 4
+// entries at high sparsity) measured faster with 8
+constexpr int kGivenDownUnroll = 8;
 
 // Lane `lane` keeps chunks lane, lane + 64, ... of x (fp32) in registers.
 template <typename WT, int NC>
@@ -778,10 +785,10 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
     for (int kd = 0; kd < NCD; ++kd)
 #pragma unroll
         for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
-    for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
-        u32x4 v[kDownUnroll][NCD];
+    for (int a0 = 0; a0 < na; a0 += kGivenDownUnroll) {
+        u32x4 v[kGivenDownUnroll][NCD];
 #pragma unroll
-        for (int u = 0; u < kDownUnroll; ++u) {
+        for (int u = 0; u < kGivenDownUnroll; ++u) {
             const int aa = a0 + u;
             const int n = __builtin_amdgcn_readfirstlane(aa < na ? s_row[s_al[aa < na ? aa : 0]] : -1);
             const __amdgpu_buffer_rsrc_t rs =
@@ -794,7 +801,7 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
             }
         }
 #pragma unroll
-        for (int u = 0; u < kDownUnroll; ++u) {
+        for (int u = 0; u < kGivenDownUnroll; ++u) {
             const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
 #pragma unroll
             for (int kd = 0; kd < NCD; ++kd) {
