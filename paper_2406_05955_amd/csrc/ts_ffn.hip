@@ -2191,7 +2191,7 @@ ts_status run_slots(const float *x, const void *wg, const void *wu, const void *
 
 ts_status check_ffn_args(const float *x, const void *wg, const void *wu, const void *wd, ts_dtype dt, int batch,
                          int hidden, int inter, const float *out, const ts_ffn_stats *stats, const void *ws,
-                         size_t ws_bytes, SlotPlan *plan) {
+                         size_t ws_bytes, SlotPlan *plan, bool pow2_tiles = true) {
     ts_status s = check_dims(batch, hidden, inter, dt);
     if (s != TS_OK) return s;
     if (!x || !wg || !wu || !wd || !out) return TS_ERR_NULL;
@@ -2199,7 +2199,7 @@ ts_status check_ffn_args(const float *x, const void *wg, const void *wu, const v
         return TS_ERR_ALIGN;
     s = check_stats(stats);
     if (s != TS_OK) return s;
-    if (!plan_slots(hidden, inter, dt, batch, 1, plan)) return TS_ERR_SHAPE;
+    if (!plan_slots(hidden, inter, dt, batch, 1, plan, pow2_tiles)) return TS_ERR_SHAPE;
     if (!ws || ws_bytes < ffn_ws_bytes(batch, hidden, inter, dt)) return TS_ERR_WORKSPACE;
     if (!aligned16(ws)) return TS_ERR_ALIGN;
     return TS_OK;
@@ -2307,7 +2307,7 @@ ts_status ts_ffn_sparse_topk(const float *x, const void *w_gate, const void *w_u
     if (keep < 0) return TS_ERR_SHAPE;
     ts::SlotPlan p;
     ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws,
-                                     ws_bytes, &p);
+                                     ws_bytes, &p, false);
     if (s != TS_OK) return s;
     if (inter > ts::kSelMax || p.gntiles * p.gtile > ts::kSelSpan || p.ntiles * p.tile > ts::kSelSpan ||
         p.gntiles > ts::kSelMaxTiles || p.ntiles > ts::kSelMaxTiles)

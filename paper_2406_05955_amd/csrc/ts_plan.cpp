@@ -52,16 +52,17 @@ int choose_tile(int inter, int slots, int cap) {
     return (int)std::min<long long>(cap, std::max<long long>(8, per));
 }
 
-// The fused kernel (the dense comparator's) unrolls each wave's rows in
-// pairs: rows per wave rounded up to a power of two leave no idle step, and
-// measured faster (56 -> 64 neurons at inter 14336: 224 workgroups, 3% less
-// time dense) as long as the grid keeps 7/8 of its target size.
-int choose_fused_tile(int inter, int slots) {
-    const int t = choose_tile(inter, slots, kMaxTile);
+// The single-token kernels unroll each wave's rows (pipelined: a power of
+// two of them, in pairs): rows per wave rounded up to a power of two leave
+// no idle step, and measured faster (56 -> 64 neurons at inter 14336, 224
+// workgroups: the dense comparator 3% less time, the sparse kernel 0.5-2.3%
+// across 50-99% sparsity) as long as the grid keeps 7/8 of its target size.
+int choose_pow2_tile(int inter, int slots, int cap) {
+    const int t = choose_tile(inter, slots, cap);
     if (tuned_tile() > 0) return t;
     int r2 = 1;
     while (r2 * kWaves < t) r2 <<= 1;
-    const int t2 = std::min(kMaxTile, r2 * kWaves);
+    const int t2 = std::min(cap, r2 * kWaves);
     const long long wgs = (long long)slots * ((inter + t2 - 1) / t2);
     return wgs * 8 >= 7LL * kTargetTiles ? t2 : t;
 }
@@ -96,7 +97,7 @@ ts_status check_stats(const ts_ffn_stats *s) {
     return TS_OK;
 }
 
-bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p) {
+bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p, bool pow2_tiles) {
     if (check_dims(1, hidden, inter, dt) != TS_OK || slots < 1 || slots_per_out < 1 ||
         slots % slots_per_out != 0)
         return false;
@@ -109,9 +110,9 @@ bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out
     int need = (q.nch + 63) / 64;
     q.nc = 1;
     while (q.nc < need) q.nc <<= 1;
-    q.tile = choose_tile(inter, slots, kMaxPipeTile);
+    q.tile = pow2_tiles ? choose_pow2_tile(inter, slots, kMaxPipeTile) : choose_tile(inter, slots, kMaxPipeTile);
     q.ntiles = (inter + q.tile - 1) / q.tile;
-    q.ftile = choose_fused_tile(inter, slots);
+    q.ftile = pow2_tiles ? choose_pow2_tile(inter, slots, kMaxTile) : choose_tile(inter, slots, kMaxTile);
     q.fntiles = (inter + q.ftile - 1) / q.ftile;
     q.slots = slots;
     q.slots_per_out = slots_per_out;
@@ -292,9 +293,10 @@ size_t given_ws_bytes(int batch, int hidden, int inter, int max_count, ts_dtype 
 // pick a path at call time, and the tuning knobs can move the choice).
 size_t ffn_ws_bytes(int batch, int hidden, int inter, ts_dtype dt) {
     if (check_dims(batch, hidden, inter, dt) != TS_OK) return 0;
-    SlotPlan sp;
-    if (!plan_slots(hidden, inter, dt, batch, 1, &sp)) return 0;
-    size_t n = sp.total;
+    SlotPlan sp, tp;
+    if (!plan_slots(hidden, inter, dt, batch, 1, &sp) || !plan_slots(hidden, inter, dt, batch, 1, &tp, false))
+        return 0;
+    size_t n = std::max(sp.total, tp.total);  // (tp: the top-k mask's plan)
     BatchPlan bp;
     if (batch > 1 && plan_batch(std::min(batch, kBxMaxTokens), hidden, inter, 1, 1, dt, &bp))
         n = std::max(n, bp.total);

@@ -109,9 +109,13 @@ size_t given_ws_bytes(int batch, int hidden, int inter, int max_count, ts_dtype 
 
 int tuned_tile();
 int choose_tile(int inter, int slots, int cap);
-int choose_fused_tile(int inter, int slots);
+int choose_pow2_tile(int inter, int slots, int cap);
 int tuned(const char *key);
-bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p);
+// pow2_tiles: the pipelined / fused kernels' tiles per choose_pow2_tile (the
+// default); false: per choose_tile (the top-k mask's sequence, measured
+// faster with the finer tiles)
+bool plan_slots(int hidden, int inter, ts_dtype dt, int slots, int slots_per_out, SlotPlan *p,
+                bool pow2_tiles = true);
 bool plan_batch(int batch, int hidden, int inter, int groups, int top_k, ts_dtype dt, BatchPlan *p);
 
 ts_status check_dims(int batch, int hidden, int inter, ts_dtype dt);
