@@ -14,6 +14,19 @@ static int fail(const char *what, int B, int H, int I, int S) {
 }
 
 int main() {
+    // the tile rule: about one workgroup per compute unit, rows per wave a
+    // power of two while the grid keeps 7/8 of its size
+    if (choose_pow2_tile(14336, 1, kMaxPipeTile) != 64) return fail("pow2 tile 14336", 0, 0, 14336, 1);
+    if (choose_pow2_tile(14336, 2, kMaxPipeTile) != 128) return fail("pow2 tile 14336 x2", 0, 0, 14336, 2);
+    if (choose_pow2_tile(9000, 1, kMaxPipeTile) != 40) return fail("pow2 tile 9000", 0, 0, 9000, 1);
+    if (choose_pow2_tile(14336, 1, kMaxTile) != 64) return fail("pow2 fused tile 14336", 0, 0, 14336, 1);
+    if (choose_tile(14336, 1, kMaxPipeTile) != 56) return fail("tile 14336", 0, 0, 14336, 1);
+    for (int I = 1; I <= 40000; I += 37)
+        for (int S : {1, 2, 3, 16}) {
+            const int t = choose_pow2_tile(I, S, kMaxPipeTile), b = choose_tile(I, S, kMaxPipeTile);
+            if (t % 8 || t < b || t > kMaxPipeTile) return fail("pow2 tile bounds", 0, 0, I, S);
+            if (t != b && (long long)S * ((I + t - 1) / t) * 8 < 7LL * kTargetTiles) return fail("pow2 tile grid", 0, 0, I, S);
+        }
     const int Hs[] = {8, 16, 40, 200, 512, 1000, 2048, 4096, 6144, 8192};
     const int Is[] = {1, 3, 7, 8, 9, 63, 64, 65, 130, 777, 1792, 3001, 14336, 28672, 100000};
     const int Ss[] = {1, 2, 3, 8, 16, 32, 64, 256, 512, 2048};
