@@ -1155,6 +1155,10 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
             if (wave == 0) sel_find_bin(s_hist, s_st, shift == 24 ? (uint32_t)k : s_st[1], shift, lane);
             mask |= 255u << shift;
             __syncthreads();
+            // every key of the chosen bin kept: the k-th largest is the bin's
+            // smallest, and the bin's floor (lower digits 0) is as good a
+            // threshold; the remaining digits are not needed
+            if (s_st[1] == s_st[2]) break;
         }
         thr = s_st[0];
         const uint32_t ties = s_st[1], neq = s_st[2];
@@ -1428,6 +1432,10 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
             if (wave == 0) sel_find_bin(s_hist, s_st, shift == 24 ? (uint32_t)k : s_st[1], shift, lane);
             mask |= 255u << shift;
             __syncthreads();
+            // every key of the chosen bin kept: the k-th largest is the bin's
+            // smallest, and the bin's floor (lower digits 0) is as good a
+            // threshold; the remaining digits are not needed
+            if (s_st[1] == s_st[2]) break;
         }
         thr = s_st[0];
         const uint32_t ties = s_st[1], neq = s_st[2];
