@@ -370,9 +370,10 @@ __global__ __launch_bounds__(kThreads) void ffn_fused(SlotArgs a) {
 // known to be open, issues that row's W_up loads; the up dot is finished one
 // row later, while the wave's next gate rows are in flight.  The up traffic
 // therefore travels with the gate stream instead of forming a burst after
-// it, and no barrier separates the two.  Then, behind one barrier, wave 0
-// ballots the open gates and the non-zero Combined activations of the tile
-// and the 512 threads run the down axpy (hidden split over threads).
+// it, and no barrier separates the two.  Then, behind one barrier, every
+// wave ballots the tile's non-zero Combined activations into its own copy
+// of the list (no second barrier) and the 512 threads run the down axpy
+// (hidden split over threads).
 
 template <typename WT, int NC>
 struct PipeWave {
@@ -447,9 +448,8 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     __shared__ float s_g[kMaxPipeTile];
     __shared__ float s_h[kMaxPipeTile];
     __shared__ int s_on[kMaxPipeTile];
-    __shared__ int s_al[kMaxPipeTile];
-    __shared__ float s_av[kMaxPipeTile];
-    __shared__ int s_n[2];
+    __shared__ int s_alw[EMIT ? 1 : kWaves][kMaxPipeTile];   // per-wave copies of the active list
+    __shared__ float s_avw[EMIT ? 1 : kWaves][kMaxPipeTile];
     __shared__ float s_logit[kMaxExperts];
     __shared__ int s_expert;
 
@@ -540,9 +540,89 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     __syncthreads();
 
     // ---- ballots: open gates (report) and non-zero Combined activations ------
+    if constexpr (!EMIT) {
+        // every wave lists the tile's rows itself (the same ballots over the
+        // same LDS data, into its own copy), so its down loads start without
+        // waiting for a second barrier
+        int *al = s_alw[wave];
+        float *av = s_avw[wave];
+        int ng = 0, na = 0;
+        for (int h = 0; h < (nt + 63) / 64; ++h) {
+            const int r = lane + 64 * h;
+            const bool in = r < nt;
+            const bool pg = in && s_g[r] > gate_threshold(a.act, a.tau);
+            const uint64_t mg = __ballot(pg);
+            if (wave == 0 && pg && a.want_seg) a.gseg[pr * a.tile + ng + lane_prefix(mg, lane)] = n0 + r * rs;
+            const bool pa = in && s_on[r];
+            const uint64_t ma = __ballot(pa);
+            if (pa) {
+                const int pos = na + lane_prefix(ma, lane);
+                al[pos] = r;
+                av[pos] = s_h[r];
+                if (wave == 0 && a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r * rs;
+            }
+            ng += __popcll(mg);
+            na += __popcll(ma);
+        }
+        __builtin_amdgcn_wave_barrier();  // the wave's list writes before its reads
+
+        // ---- down: axpy over the W_down_t rows of A, hidden split over threads
+        float acc[NCD][CE];
+#pragma unroll
+        for (int kd = 0; kd < NCD; ++kd)
+#pragma unroll
+            for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
+        const __amdgpu_buffer_rsrc_t rd = make_rsrc(wd, tbytes);
+        for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
+            u32x4 v[kDownUnroll][NCD];
+#pragma unroll
+            for (int u = 0; u < kDownUnroll; ++u) {
+                const int aa = a0 + u;
+                const uint32_t base =
+                    aa < na ? (uint32_t)al[aa] * (uint32_t)(H * rs) * (uint32_t)sizeof(WT) : kOutOfRange;
+#pragma unroll
+                for (int kd = 0; kd < NCD; ++kd) {
+                    const int c = tid + kThreads * kd;
+                    v[u][kd] = ld_buf_stream(rd, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kDownUnroll; ++u) {
+                const float hv = a0 + u < na ? av[a0 + u] : 0.f;
+#pragma unroll
+                for (int kd = 0; kd < NCD; ++kd) {
+                    float f[CE];
+                    unpack<WT>(v[u][kd], f);
+#pragma unroll
+                    for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
+                }
+            }
+        }
+        float *prow = a.partial + pr * H;
+#pragma unroll
+        for (int kd = 0; kd < NCD; ++kd) {
+            const int c = tid + kThreads * kd;
+            if (c < nch) {
+#pragma unroll
+                for (int e = 0; e < CE; e += 4)
+                    *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
+                        f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
+            }
+        }
+        if (tid == 0) {
+            a.cnt[pr * 2] = ng;
+            a.cnt[pr * 2 + 1] = na;
+        }
+        return;
+    }
+
+    // ---- emit mode: wave 0 lists the tile's open gates (report) and its
+    // non-zero Combined activations with their values for the kernel that
+    // decides which of them enter the down projection
+    __shared__ int s_n[2];
     if (wave == 0) {
-        int ng = 0, na0 = 0;
-        for (int h = 0; h < kMaxPipeTile / 64; ++h) {
+        int ng = 0, na = 0;
+        for (int h = 0; h < (nt + 63) / 64; ++h) {
             const int r = lane + 64 * h;
             const bool in = r < nt;
             const bool pg = in && s_g[r] > gate_threshold(a.act, a.tau);
@@ -551,78 +631,22 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
             const bool pa = in && s_on[r];
             const uint64_t ma = __ballot(pa);
             if (pa) {
-                const int pos = na0 + lane_prefix(ma, lane);
-                s_al[pos] = r;
-                s_av[pos] = s_h[r];
-                if (EMIT || a.want_seg) a.aseg[pr * a.tile + pos] = n0 + r * rs;
-                if (EMIT) a.hseg[pr * a.tile + pos] = s_h[r];
+                const int pos = na + lane_prefix(ma, lane);
+                a.aseg[pr * a.tile + pos] = n0 + r * rs;
+                a.hseg[pr * a.tile + pos] = s_h[r];
             }
             ng += __popcll(mg);
-            na0 += __popcll(ma);
+            na += __popcll(ma);
         }
         if (lane == 0) {
             s_n[0] = ng;
-            s_n[1] = na0;
+            s_n[1] = na;
+            a.cnt[pr * 2] = ng;
+            a.cnt[pr * 2 + 1] = na;
         }
     }
     __syncthreads();
-    const int na = s_n[1];
-    if constexpr (EMIT) {
-        if (tid == 0) {
-            a.cnt[pr * 2] = s_n[0];
-            a.cnt[pr * 2 + 1] = na;
-        }
-        for (int q = na + tid; q < a.tile; q += kThreads) a.aseg[pr * a.tile + q] = -1;  // padding
-        return;
-    }
-
-    // ---- down: axpy over the W_down_t rows of A, hidden split over threads --
-    float acc[NCD][CE];
-#pragma unroll
-    for (int kd = 0; kd < NCD; ++kd)
-#pragma unroll
-        for (int e = 0; e < CE; ++e) acc[kd][e] = 0.f;
-    const __amdgpu_buffer_rsrc_t rd = make_rsrc(wd, tbytes);
-    for (int a0 = 0; a0 < na; a0 += kDownUnroll) {
-        u32x4 v[kDownUnroll][NCD];
-#pragma unroll
-        for (int u = 0; u < kDownUnroll; ++u) {
-            const int aa = a0 + u;
-            const uint32_t base =
-                aa < na ? (uint32_t)s_al[aa] * (uint32_t)(H * rs) * (uint32_t)sizeof(WT) : kOutOfRange;
-#pragma unroll
-            for (int kd = 0; kd < NCD; ++kd) {
-                const int c = tid + kThreads * kd;
-                v[u][kd] = ld_buf_stream(rd, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kDownUnroll; ++u) {
-            const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
-#pragma unroll
-            for (int kd = 0; kd < NCD; ++kd) {
-                float f[CE];
-                unpack<WT>(v[u][kd], f);
-#pragma unroll
-                for (int e = 0; e < CE; ++e) acc[kd][e] = fmaf(hv, f[e], acc[kd][e]);
-            }
-        }
-    }
-    float *prow = a.partial + pr * H;
-#pragma unroll
-    for (int kd = 0; kd < NCD; ++kd) {
-        const int c = tid + kThreads * kd;
-        if (c < nch) {
-#pragma unroll
-            for (int e = 0; e < CE; e += 4)
-                *reinterpret_cast<f32x4 *>(prow + c * CE + e) =
-                    f32x4{acc[kd][e], acc[kd][e + 1], acc[kd][e + 2], acc[kd][e + 3]};
-        }
-    }
-    if (tid == 0) {
-        a.cnt[pr * 2] = s_n[0];
-        a.cnt[pr * 2 + 1] = na;
-    }
+    for (int q = s_n[1] + tid; q < a.tile; q += kThreads) a.aseg[pr * a.tile + q] = -1;  // padding
 }
 
 // ---------------------------------------------------------------------------
