@@ -733,9 +733,8 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
     __shared__ float s_g[kMaxPipeTile];
     __shared__ float s_h[kMaxPipeTile];
     __shared__ int s_on[kMaxPipeTile];
-    __shared__ int s_al[kMaxPipeTile];
-    __shared__ float s_av[kMaxPipeTile];
-    __shared__ int s_n[2];
+    __shared__ int s_alw[kWaves][kMaxPipeTile];  // per-wave copies of the active list
+    __shared__ float s_avw[kWaves][kMaxPipeTile];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -778,30 +777,26 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
     }
     __syncthreads();
 
-    // ---- ballots: entries with an open gate (count) and non-zero Combined ----
-    if (wave == 0) {
-        int ng = 0, na0 = 0;
-        for (int h = 0; h < kMaxPipeTile / 64; ++h) {
-            const int r = lane + 64 * h;
-            const bool in = r < nt && s_row[r] >= 0;
-            const uint64_t mg = __ballot(in && s_g[r] > 0.f);
-            const bool pa = in && s_on[r];
-            const uint64_t ma = __ballot(pa);
-            if (pa) {
-                const int pos = na0 + lane_prefix(ma, lane);
-                s_al[pos] = r;
-                s_av[pos] = s_h[r];
-            }
-            ng += __popcll(mg);
-            na0 += __popcll(ma);
+    // ---- ballots: entries with an open gate (count) and non-zero Combined;
+    // every wave lists them itself, into its own copy (no second barrier)
+    int *al = s_alw[wave];
+    float *av = s_avw[wave];
+    int ng = 0, na = 0;
+    for (int h = 0; h < (nt + 63) / 64; ++h) {
+        const int r = lane + 64 * h;
+        const bool in = r < nt && s_row[r] >= 0;
+        const uint64_t mg = __ballot(in && s_g[r] > 0.f);
+        const bool pa = in && s_on[r];
+        const uint64_t ma = __ballot(pa);
+        if (pa) {
+            const int pos = na + lane_prefix(ma, lane);
+            al[pos] = r;
+            av[pos] = s_h[r];
         }
-        if (lane == 0) {
-            s_n[0] = ng;
-            s_n[1] = na0;
-        }
+        ng += __popcll(mg);
+        na += __popcll(ma);
     }
-    __syncthreads();
-    const int na = s_n[1];
+    __builtin_amdgcn_wave_barrier();  // the wave's list writes before its reads
 
     // ---- down: axpy over the W_down_t rows of the non-zero entries ----------
     float acc[NCD][CE];
@@ -814,7 +809,7 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
 #pragma unroll
         for (int u = 0; u < kGivenDownUnroll; ++u) {
             const int aa = a0 + u;
-            const int n = __builtin_amdgcn_readfirstlane(aa < na ? s_row[s_al[aa < na ? aa : 0]] : -1);
+            const int n = __builtin_amdgcn_readfirstlane(aa < na ? s_row[al[aa < na ? aa : 0]] : -1);
             const __amdgpu_buffer_rsrc_t rs =
                 make_rsrc(n >= 0 ? static_cast<const void *>(wd + (size_t)(n >= 0 ? n : 0) * H) : xt,
                           n >= 0 ? (uint32_t)H * (uint32_t)sizeof(WT) : 0u);
@@ -826,7 +821,7 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
         }
 #pragma unroll
         for (int u = 0; u < kGivenDownUnroll; ++u) {
-            const float hv = a0 + u < na ? s_av[a0 + u] : 0.f;
+            const float hv = a0 + u < na ? av[a0 + u] : 0.f;
 #pragma unroll
             for (int kd = 0; kd < NCD; ++kd) {
                 float f[CE];
@@ -848,7 +843,7 @@ __global__ __launch_bounds__(kThreads) void ffn_given(GivenArgs a) {
         }
     }
     if (tid == 0) {
-        a.cnt[pr * 2] = s_n[0];
+        a.cnt[pr * 2] = ng;
         a.cnt[pr * 2 + 1] = na;
     }
 }
