@@ -51,9 +51,9 @@
 namespace ts {
 
 // W_down_t rows whose loads are in flight together in the down phases: 16
-// covers the active rows of all but ~0.1% of 56-neuron tiles at 90%
-// sparsity in one round trip (8 left ~9% of the tiles a second one, and the
-// slowest tile sets the kernel's end: 0.2 us per layer)
+// covers the active rows of nearly every 56- or 64-neuron tile at 90%
+// sparsity in one round trip (with 8, ~9% of 56-neuron tiles needed a
+// second one, and the slowest tile sets the kernel's end: 0.2 us per layer)
 constexpr int kDownUnroll = 16;
 // ffn_given builds a buffer resource per row; its short chunks (often 4
 // entries at high sparsity) measured faster with 8
