@@ -287,8 +287,9 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *   "rif"        weight rows in flight per wave in the row dot products
  *                (1 or 2)
  *   "bx_gate"    load shape of the batched gate+up kernel for up to 16
- *                tokens per group: 0 default (4 k-steps of 32 per batch, 2
- *                batches in flight), 1 = 2 x 2, 2 = 2 x 4
+ *                tokens per group: 0 default (k-steps of 32 per batch x
+ *                batches in flight: 2 x 2 for up to 8 tokens, 4 x 2 for 16),
+ *                1 = 2 x 2, 2 = 2 x 4
  *   "bx_down"    batched down kernel for up to 32 tokens per group: 0 default
  *                (2 blocks of 32 rows in flight per wave), 1 = 3 blocks
  *   "bx_vgroup"  batched MoE layer: 0 default (token slots per expert group

@@ -72,7 +72,9 @@ struct Bx {
     static constexpr bool PACK = TOK == 8;          // high and low parts share one 16-column tile
     static constexpr int NT = PACK ? 1 : TOK / 16;  // 16-token accumulator tiles
     static constexpr int NX = PACK ? 1 : 2 * NT;    // operand fragments per 32-wide k-step (x or Combined)
-    static constexpr int KS = NX <= 2 ? 4 : 2;      // k-steps per batch of gate / up loads (default)
+    // k-steps per batch of gate / up loads (default; measured: 2 at 8 token
+    // slots, 4 at 16, 2 past that, where deeper rings spill)
+    static constexpr int KS = PACK ? 2 : (NX <= 2 ? 4 : 2);
     static constexpr int D = 2;                     // gate / up batches in flight per wave (default)
     static constexpr int DD = 2;                    // down blocks in flight per wave (default)
 };
