@@ -114,9 +114,41 @@ def wdtype_of(t: torch.Tensor) -> int:
 
 
 def _need_cuda(*ts):
+    dev = None
     for t in ts:
-        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+        if t is None:
+            continue
+        if not t.is_cuda or not t.is_contiguous():
             raise ValueError("tensors must be contiguous device tensors")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"tensors on different devices ({dev}, {t.device})")
+
+
+def _check_tensors(x, w_gate, w_up, w_down_t, out, w_router=None):
+    """What the C ABI cannot check (it sees only pointers and the sizes passed
+    with them): x float32 [B][H]; W_gate, W_up, W_down_t one dtype and one
+    shape, [I][H] or, for the MoE layer, [E][I][H] with the router [E][H] of
+    the same dtype; out float32 [B][H]; all contiguous on one device.  A
+    mismatch here would let the kernels read or write past a buffer."""
+    if x.dtype != torch.float32 or x.dim() != 2:
+        raise TypeError(f"x must be a float32 [batch][hidden] tensor, got {x.dtype} {tuple(x.shape)}")
+    B, H = x.shape
+    moe = w_router is not None
+    wdtype_of(w_gate)
+    if w_gate.dim() != (3 if moe else 2) or w_gate.shape[-1] != H:
+        raise ValueError(f"w_gate must be [{'experts][' if moe else ''}inter][{H}], got {tuple(w_gate.shape)}")
+    for name, w in (("w_up", w_up), ("w_down_t", w_down_t)):
+        if w.dtype != w_gate.dtype or w.shape != w_gate.shape:
+            raise ValueError(f"{name} must match w_gate ({w_gate.dtype} {tuple(w_gate.shape)}), "
+                             f"got {w.dtype} {tuple(w.shape)}")
+    if moe and (w_router.dtype != w_gate.dtype or tuple(w_router.shape) != (w_gate.shape[0], H)):
+        raise ValueError(f"w_router must be {w_gate.dtype} [{w_gate.shape[0]}][{H}], "
+                         f"got {w_router.dtype} {tuple(w_router.shape)}")
+    if out is not None and (out.dtype != torch.float32 or tuple(out.shape) != (B, H)):
+        raise ValueError(f"out must be float32 [{B}][{H}], got {out.dtype} {tuple(out.shape)}")
+    _need_cuda(x, out, w_gate, w_up, w_down_t, w_router)
 
 
 def ffn_workspace_bytes(batch: int, hidden: int, inter: int, wdtype: int) -> int:
@@ -132,9 +164,18 @@ def moe_workspace_bytes(batch: int, hidden: int, inter: int, n_experts: int, top
 
 
 def _workspace(nbytes: int, device, ws):
+    """The caller's workspace (any dtype; its size in bytes is passed on), or
+    a new one of the size the library asks for."""
     if ws is not None:
+        _need_cuda(ws)
+        if ws.device != device:
+            raise ValueError(f"workspace on {ws.device}, tensors on {device}")
         return ws
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
 
 
 def _stats_struct(batch_slots: int, inter: int, device, want: bool):
@@ -154,7 +195,7 @@ def ffn_sparse(x, w_gate, w_up, w_down_t, out=None, stats: bool = False, union: 
                stream=None):
     """ts_ffn_sparse.  x [B][H] f32; weights [I][H] f32/bf16.  Returns out, or
     (out, stats dict) when stats/union is requested."""
-    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
     B, H = x.shape
     I = w_gate.shape[0]
     dt = wdtype_of(w_gate)
@@ -166,7 +207,7 @@ def ffn_sparse(x, w_gate, w_up, w_down_t, out=None, stats: bool = False, union: 
         d["n_union"] = torch.empty(2, dtype=torch.int32, device=x.device)
         st.n_union = _ptr(d["n_union"])
     code = lib.ts_ffn_sparse(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out),
-                             ctypes.byref(st) if st is not None else None, _ptr(ws), ws.numel(), _stream(stream))
+                             ctypes.byref(st) if st is not None else None, _ptr(ws), _nbytes(ws), _stream(stream))
     _check(code, "ts_ffn_sparse")
     return (out, d) if d is not None else out
 
@@ -179,7 +220,7 @@ def ffn_sparse_act(x, w_gate, w_up, w_down_t, act: int, tau: float = 0.0, out=No
                    union: bool = False, ws=None, stream=None):
     """ts_ffn_sparse_act: act TS_ACT_DRELU (tau 0) or TS_ACT_RELU_GATE
     (Combined = max(0, gate - tau) * up).  Returns out, or (out, stats dict)."""
-    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
     B, H = x.shape
     I = w_gate.shape[0]
     dt = wdtype_of(w_gate)
@@ -192,7 +233,7 @@ def ffn_sparse_act(x, w_gate, w_up, w_down_t, act: int, tau: float = 0.0, out=No
         st.n_union = _ptr(d["n_union"])
     code = lib.ts_ffn_sparse_act(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, int(act),
                                  float(tau), _ptr(out), ctypes.byref(st) if st is not None else None, _ptr(ws),
-                                 ws.numel(), _stream(stream))
+                                 _nbytes(ws), _stream(stream))
     _check(code, "ts_ffn_sparse_act")
     return (out, d) if d is not None else out
 
@@ -200,7 +241,7 @@ def ffn_sparse_act(x, w_gate, w_up, w_down_t, act: int, tau: float = 0.0, out=No
 def ffn_sparse_topk(x, w_gate, w_up, w_down_t, keep: int, out=None, stats: bool = False, ws=None, stream=None):
     """ts_ffn_sparse_topk: dReLU FFN keeping each token's `keep` largest
     Combined activations.  Returns out, or (out, stats dict)."""
-    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
     B, H = x.shape
     I = w_gate.shape[0]
     dt = wdtype_of(w_gate)
@@ -209,7 +250,7 @@ def ffn_sparse_topk(x, w_gate, w_up, w_down_t, keep: int, out=None, stats: bool 
     ws = _workspace(ffn_workspace_bytes(B, H, I, dt), x.device, ws)
     st, d = _stats_struct(B, I, x.device, stats)
     code = lib.ts_ffn_sparse_topk(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, int(keep),
-                                  _ptr(out), ctypes.byref(st) if st is not None else None, _ptr(ws), ws.numel(),
+                                  _ptr(out), ctypes.byref(st) if st is not None else None, _ptr(ws), _nbytes(ws),
                                   _stream(stream))
     _check(code, "ts_ffn_sparse_topk")
     return (out, d) if d is not None else out
@@ -217,7 +258,7 @@ def ffn_sparse_topk(x, w_gate, w_up, w_down_t, keep: int, out=None, stats: bool 
 
 def ffn_dense(x, w_gate, w_up, w_down_t, out=None, ws=None, stream=None):
     """ts_ffn_dense (all neurons, all three matrices read)."""
-    _need_cuda(x, w_gate, w_up, w_down_t, out)
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
     B, H = x.shape
     I = w_gate.shape[0]
     dt = wdtype_of(w_gate)
@@ -225,7 +266,7 @@ def ffn_dense(x, w_gate, w_up, w_down_t, out=None, ws=None, stream=None):
         out = torch.empty(B, H, dtype=torch.float32, device=x.device)
     ws = _workspace(ffn_workspace_bytes(B, H, I, dt), x.device, ws)
     code = lib.ts_ffn_dense(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out), _ptr(ws),
-                            ws.numel(), _stream(stream))
+                            _nbytes(ws), _stream(stream))
     _check(code, "ts_ffn_dense")
     return out
 
@@ -234,7 +275,8 @@ def ffn_sparse_given(x, w_gate, w_up, w_down_t, idx, count, out=None, stats: boo
     """ts_ffn_sparse_given: the FFN over given neuron lists.  idx int32
     [B][max_count], count int32 [B] (device tensors).  Returns out, or (out,
     {"n_gate", "n_active"}) with stats=True."""
-    _need_cuda(x, w_gate, w_up, w_down_t, out, idx, count)
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
+    _need_cuda(x, idx, count)
     B, H = x.shape
     I = w_gate.shape[0]
     dt = wdtype_of(w_gate)
@@ -253,7 +295,7 @@ def ffn_sparse_given(x, w_gate, w_up, w_down_t, idx, count, out=None, stats: boo
         st = ffn_stats_t(_ptr(d["n_gate"]), _ptr(d["n_active"]), None, None, None)
     code = lib.ts_ffn_sparse_given(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(idx),
                                    _ptr(count), maxc, _ptr(out), ctypes.byref(st) if st is not None else None,
-                                   _ptr(ws), ws.numel(), _stream(stream))
+                                   _ptr(ws), _nbytes(ws), _stream(stream))
     _check(code, "ts_ffn_sparse_given")
     return (out, d) if d is not None else out
 
@@ -262,7 +304,7 @@ def moe_sparse(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, stats:
                stream=None, dense: bool = False):
     """ts_moe_sparse (or ts_moe_dense with dense=True).  Returns
     (out, topk_idx, topk_w) or (out, topk_idx, topk_w, stats dict)."""
-    _need_cuda(x, w_router, w_gate, w_up, w_down_t, out)
+    _check_tensors(x, w_gate, w_up, w_down_t, out, w_router=w_router)
     B, H = x.shape
     E, I = w_gate.shape[0], w_gate.shape[1]
     dt = wdtype_of(w_gate)
@@ -273,13 +315,13 @@ def moe_sparse(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, stats:
     ws = _workspace(moe_workspace_bytes(B, H, I, E, top_k, dt), x.device, ws)
     if dense:
         code = lib.ts_moe_dense(_ptr(x), _ptr(w_router), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, E,
-                                top_k, _ptr(out), _ptr(idx), _ptr(wts), _ptr(ws), ws.numel(), _stream(stream))
+                                top_k, _ptr(out), _ptr(idx), _ptr(wts), _ptr(ws), _nbytes(ws), _stream(stream))
         _check(code, "ts_moe_dense")
         return out, idx, wts
     st, d = _stats_struct(B * top_k, I, x.device, stats)
     code = lib.ts_moe_sparse(_ptr(x), _ptr(w_router), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, E,
                              top_k, _ptr(out), _ptr(idx), _ptr(wts), ctypes.byref(st) if st is not None else None,
-                             _ptr(ws), ws.numel(), _stream(stream))
+                             _ptr(ws), _nbytes(ws), _stream(stream))
     _check(code, "ts_moe_sparse")
     return (out, idx, wts, d) if d is not None else (out, idx, wts)
 
@@ -289,13 +331,19 @@ def moe_dense(x, w_router, w_gate, w_up, w_down_t, top_k: int, out=None, ws=None
 
 
 def probe_read(src: torch.Tensor, sink: torch.Tensor, stream=None):
-    _check(lib.ts_probe_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)),
-           "ts_probe_read")
+    """ts_probe_read: sink holds one float32 per workgroup (4096)."""
+    if sink.dtype != torch.float32 or sink.numel() < 4096:
+        raise ValueError("sink must be float32 with at least 4096 elements")
+    _need_cuda(src, sink)
+    _check(lib.ts_probe_read(_ptr(src), _nbytes(src), _ptr(sink), _stream(stream)), "ts_probe_read")
 
 
 def probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
-    _check(lib.ts_probe_copy(_ptr(src), _ptr(dst), src.numel() * src.element_size(), _stream(stream)),
-           "ts_probe_copy")
+    """ts_probe_copy: copies all of src into the start of dst."""
+    if _nbytes(dst) < _nbytes(src):
+        raise ValueError("dst is smaller than src")
+    _need_cuda(src, dst)
+    _check(lib.ts_probe_copy(_ptr(src), _ptr(dst), _nbytes(src), _stream(stream)), "ts_probe_copy")
 
 
 def prof_enable(on: bool):
