@@ -32,6 +32,16 @@ hipEvent_t take_event() {
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     return e;
 }
+
+// Both events of a record, or neither (a half-made pair goes back to the pool).
+bool take_pair(ProfRecord &r) {
+    r.start = take_event();
+    r.stop = take_event();
+    if (r.start && r.stop) return true;
+    if (r.start) g_pool.push_back(r.start);
+    if (r.stop) g_pool.push_back(r.stop);
+    return false;
+}
 }  // namespace
 
 void set_last_error(const char *where, hipError_t e) {
@@ -52,9 +62,7 @@ bool prof_events(const char *kernel, hipEvent_t *start, hipEvent_t *stop) {
     if (!g_prof_on) return false;
     ProfRecord r;
     r.kernel = kernel;
-    r.start = take_event();
-    r.stop = take_event();
-    if (!r.start || !r.stop) return false;
+    if (!take_pair(r)) return false;
     g_prof.push_back(r);
     *start = r.start;
     *stop = r.stop;
@@ -66,10 +74,12 @@ ProfScope::ProfScope(const char *kernel, hipStream_t stream) : stream_(stream) {
     if (!g_prof_on) return;
     ProfRecord r;
     r.kernel = kernel;
-    r.start = take_event();
-    r.stop = take_event();
-    if (!r.start || !r.stop) return;
-    if (hipEventRecord(r.start, stream) != hipSuccess) return;
+    if (!take_pair(r)) return;
+    if (hipEventRecord(r.start, stream) != hipSuccess) {
+        g_pool.push_back(r.start);
+        g_pool.push_back(r.stop);
+        return;
+    }
     g_prof.push_back(r);
     slot_ = (int)g_prof.size() - 1;
 }
