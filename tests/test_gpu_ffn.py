@@ -208,3 +208,18 @@ def test_interleaved_tiles(dtype, B, H, I, path):
             n = int(st_i[cnt][t])
             assert torch.equal(st_i[lst][t, :n], st_c[lst][t, :n]), (lst, t)
     assert rel_l2(out_i.cpu().numpy(), out_c.cpu().numpy().astype(np.float64)) <= 1e-6
+
+
+@pytest.mark.parametrize("I", [131072, 131073])
+@pytest.mark.parametrize("path", [0, 2])
+def test_interleave_limit(I, path):
+    """At inter 131072 the tiles still interleave (the activity report merges
+    them through LDS bitmaps of that many bits); one neuron more and the
+    entry point falls back to contiguous tiles by itself.  Both sides of the
+    limit match the oracle, sets included."""
+    inp = synth.make_ffn(2, 64, I, gate_bias=-0.84, dtype=synth.BF16, seed=[83, I, path])
+    ts.tune_set("ffn_path", path)
+    try:
+        check_ffn(inp)
+    finally:
+        ts.tune_set("ffn_path", 0)
