@@ -1439,7 +1439,11 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
     const int k = min(ta.keep, n);
     uint32_t thr = 0xffffffffu;  // no key reaches it: nothing kept (k = 0)
     int tie_n = -1;              // largest kept neuron index among keys equal to thr
-    if (k > 0) {
+    if (k > 0 && k == n) {
+        // every listed entry kept (their keys are >= 0): no search
+        thr = 0u;
+        tie_n = 0x7fffffff;
+    } else if (k > 0) {
         uint32_t mask = 0u;
         for (int shift = 24; shift >= 0; shift -= 8) {
             const uint32_t prefix = s_st[0];
