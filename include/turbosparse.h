@@ -67,7 +67,7 @@ typedef enum {
     TS_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
     TS_ERR_WORKSPACE = 5,   /* ws is NULL or ws_bytes is below the required size */
     TS_ERR_HIP = 6,         /* a HIP runtime call or kernel launch failed */
-    TS_ERR_UNSUPPORTED = 7  /* valid request this build does not serve (e.g. stats on a dense call) */
+    TS_ERR_UNSUPPORTED = 7  /* valid request the library does not serve (e.g. stats on a dense call) */
 } ts_status;
 
 typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;

@@ -335,7 +335,7 @@ const char *ts_status_str(ts_status s) {
     case TS_ERR_ALIGN: return "TS_ERR_ALIGN: pointer not aligned";
     case TS_ERR_WORKSPACE: return "TS_ERR_WORKSPACE: workspace missing or too small";
     case TS_ERR_HIP: return "TS_ERR_HIP: HIP runtime failure";
-    case TS_ERR_UNSUPPORTED: return "TS_ERR_UNSUPPORTED: request not served by this build";
+    case TS_ERR_UNSUPPORTED: return "TS_ERR_UNSUPPORTED: request not served by the library";
     }
     return "unknown ts_status";
 }
