@@ -1153,7 +1153,7 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
                 s_cp[base] = (uint16_t)e;
                 s_ci[base] = (uint16_t)ai[u];
                 ++base;
-                atomicAdd(&s_hist[key >> kSelTopShift], 1u);
+                atomicAdd(&s_hist[(key >> kSelTopShift) & 255u], 1u);
             }
         }
 #pragma unroll
