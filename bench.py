@@ -13,13 +13,18 @@ so every step streams its weights from HBM.
 Prints one JSON line: tokens/s/layer = batch * layers / (seconds per step),
 the dense comparator (ts_ffn_dense) on the same stack, the roofline of the
 dominant kernel (ffn_main, the pipelined single-token kernel) from
-per-launch HIP events, and the fp64 oracle
-timed on the host cores as a CPU baseline.
+per-launch HIP events (and, when the committed rocprofv3 trace summary was
+taken on the current kernel source, from the trace as well), the fp64 oracle
+timed on the host cores as a CPU baseline, and under "configs" every other
+workload configuration with its own parity against the oracle: the small
+fp32 layer, batch 8 and 32, the MoE layer at batch 1 and 16, and the
+50-99% sparsity sweep (shorter runs: --config-steps).
 
-Other workloads (--workload): sweep (gate bias for 50/75/90/95/99% sparsity),
-moe (Mixtral-shaped top-2 MoE layer, batch 1, 16, 32, 64), batch (batch 8 and 32),
-given (predictor mode: each layer called with its exact gate set as the
-neuron list), act (dReLU beside ReGLU and the shifted gate-only ReLU).
+Other workloads (--workload, one JSON line each): sweep (gate bias for
+50/75/90/95/99% sparsity), moe (Mixtral-shaped top-2 MoE layer, batch 1, 16,
+32, 64), batch (batch 8 and 32), given (predictor mode: each layer called
+with its exact gate set as the neuron list), act (dReLU beside ReGLU and the
+shifted gate-only ReLU), topk (the top-k magnitude mask).
 """
 from __future__ import annotations
 
@@ -39,6 +44,7 @@ H_MISTRAL, I_MISTRAL = 4096, 14336
 KERNEL_SOURCES = ["paper_2406_05955_amd/csrc/ts_ffn.hip", "paper_2406_05955_amd/csrc/ts_device.h",
                   "paper_2406_05955_amd/csrc/ts_plan.cpp", "paper_2406_05955_amd/csrc/ts_plan.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_ffn_main_mistral_b1.txt")
+TRACE_FILE = os.path.join(ROOT, "profiles", "trace_ffn_main_mistral_b1.txt")
 
 
 def parse_args():
@@ -55,6 +61,11 @@ def parse_args():
     ap.add_argument("--probe", action="store_true", help="also run the HBM read / copy probes")
     ap.add_argument("--tile", type=int, default=0, help="ffn_tile tuning knob (0 = default)")
     ap.add_argument("--tune", default="", help="further tuning knobs, KEY=VALUE[,KEY=VALUE...] (ts_tune_set)")
+    ap.add_argument("--no-parity", action="store_true", help="skip the oracle parity of the other workloads")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="default workload: skip the other configurations (small fp32 layer, batch, MoE, sweep)")
+    ap.add_argument("--config-steps", type=int, default=10, help="timed steps of each other configuration")
+    ap.add_argument("--config-warmup", type=int, default=3, help="warm-up steps of each other configuration")
     ap.add_argument("--batch-sizes", default="8,32", help="batch workload: batch sizes")
     ap.add_argument("--variants", default="independent,hot_cold", help="batch workload: token generators")
     return ap.parse_args()
@@ -68,20 +79,37 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic():
-    """HBM bytes per launch of ffn_main from the committed counter summary,
-    or None if it is missing or was taken on a different kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def read_summary(path):
+    """The `key: value` lines of a committed profile summary, or None if it
+    is missing or was taken on a different kernel source."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
     if kv.get("kernel_source_sha256_16") != kernel_hash():
         return None
+    return kv
+
+
+def read_traffic():
+    """HBM bytes per launch of ffn_main from the committed counter summary,
+    or None if it is missing or was taken on a different kernel source."""
+    kv = read_summary(TRAFFIC_FILE)
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv["hbm_bytes_per_launch"]) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def read_trace():
+    """ffn_main's average launch duration (us) in the committed rocprofv3
+    kernel trace of this benchmark, or None (missing, other source)."""
+    kv = read_summary(TRACE_FILE)
+    try:
+        return (float(kv["ffn_main_avg_us"]), float(kv["ffn_reduce_avg_us"])) if kv else None
     except (KeyError, ValueError):
         return None
 
@@ -89,14 +117,16 @@ def read_traffic():
 class Stack:
     """Device-resident FFN layers and pre-marshalled C-ABI argument tuples."""
 
-    def __init__(self, ts, synth, layers, batch, hidden, inter, gate_bias, seed=0):
+    def __init__(self, ts, synth, layers, batch, hidden, inter, gate_bias, seed=0, dtype=None):
         import torch
-        self.ts, self.torch = ts, torch
+        self.ts, self.torch, self.synth = ts, torch, synth
+        self.dtype = synth.BF16 if dtype is None else dtype
+        self.esz = 2 if self.dtype == synth.BF16 else 4
         self.L, self.B, self.H, self.I = layers, batch, hidden, inter
         self.data = synth.make_ffn_stack_torch(layers, batch, hidden, inter, gate_bias=gate_bias,
-                                               dtype=synth.BF16, seed=seed, device="cuda")
+                                               dtype=self.dtype, seed=seed, device="cuda")
         self.out = torch.empty(layers, batch, hidden, dtype=torch.float32, device="cuda")
-        self.wsb = ts.ffn_workspace_bytes(batch, hidden, inter, ts.TS_BF16)
+        self.wsb = ts.ffn_workspace_bytes(batch, hidden, inter, self.dtype)
         self.ws = torch.empty(self.wsb, dtype=torch.uint8, device="cuda")
         self.stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
         vp = ctypes.c_void_p
@@ -104,7 +134,7 @@ class Stack:
         for l in range(layers):
             d = self.data
             self.args.append((vp(d["x"][l].data_ptr()), vp(d["w_gate"][l].data_ptr()), vp(d["w_up"][l].data_ptr()),
-                              vp(d["w_down_t"][l].data_ptr()), ts.TS_BF16, batch, hidden, inter,
+                              vp(d["w_down_t"][l].data_ptr()), self.dtype, batch, hidden, inter,
                               vp(self.out[l].data_ptr())))
 
     def step_sparse(self):
@@ -176,14 +206,20 @@ def _cpu_model() -> str:
 def _layer_host(stack, synth, l):
     d = stack.data
     x = d["x"][l].cpu().numpy()
-    w = [synth.tensor_to_host_array(d[k][l], synth.BF16) for k in ("w_gate", "w_up", "w_down_t")]
+    w = [synth.tensor_to_host_array(d[k][l], stack.dtype) for k in ("w_gate", "w_up", "w_down_t")]
     return x, w
+
+
+def _rel_l2(got, want) -> float:
+    import numpy as np
+    got = np.asarray(got, np.float64)
+    n = float(np.linalg.norm(want))
+    return float(np.linalg.norm(got - want) / n) if n > 0 else float(np.abs(got).max())
 
 
 def parity_layers(ts, torch, stack, synth, layers):
     """The sparse path's output of the given stack layers, recomputed into
     fresh buffers, against the fp64 oracle (relative L2 per layer)."""
-    import numpy as np
     import oracle
     d = stack.data
     rel = {}
@@ -191,9 +227,8 @@ def parity_layers(ts, torch, stack, synth, layers):
         out = ts.ffn_sparse(d["x"][l], d["w_gate"][l], d["w_up"][l], d["w_down_t"][l])
         torch.cuda.synchronize()
         x, (wg, wu, wd) = _layer_host(stack, synth, l)
-        ref = oracle.ffn(x, wg, wu, wd, synth.BF16, threads=oracle.max_threads())
-        got = out.cpu().numpy().astype(np.float64)
-        rel[l] = float(np.linalg.norm(got - ref.y) / np.linalg.norm(ref.y))
+        ref = oracle.ffn(x, wg, wu, wd, stack.dtype, threads=oracle.max_threads())
+        rel[l] = _rel_l2(out.cpu().numpy(), ref.y)
     return rel
 
 
@@ -248,7 +283,13 @@ def roofline_main(ts, torch, stack, counts, steps):
     H, I, B, L = stack.H, stack.I, stack.B, stack.L
     n_m, m_ms = kernel_avg_ms(ts, torch, stack.step_sparse, steps, "ffn_main")
     n_r, r_ms = kernel_avg_ms(ts, torch, stack.step_sparse, steps, "ffn_reduce")
-    alg = sum(bytes_sparse(2, H, I, ng, na, B) for ng, na in counts) / L
+    alg = sum(bytes_sparse(stack.esz, H, I, ng, na, B) for ng, na in counts) / L
+    if n_m == 0 or m_ms <= 0:
+        # another kernel sequence (tuning knobs, rows too wide for the
+        # pipelined kernel): no ffn_main launch to divide by
+        return {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": None,
+                "traffic": None, "kernel": "ffn_main", "launches": 0, "algorithmic_bytes_per_launch": alg,
+                "note": "no ffn_main launch recorded in this kernel sequence"}
     ach = alg / (m_ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBPS,
             "traffic": read_traffic(), "kernel": "ffn_main", "avg_launch_us": m_ms * 1e3, "launches": n_m,
@@ -292,7 +333,16 @@ def run_mistral(args, ts, synth, torch):
     # one layer's W_gate (117 MB) per launch, over the stack's layers
     ach_read = achievable_read(ts, torch, list(stack.data["w_gate"]))
     res["roofline"]["achievable_GBps"] = ach_read
-    res["roofline"]["frac_of_achievable"] = res["roofline"]["achieved"] / ach_read
+    if res["roofline"]["achieved"]:
+        res["roofline"]["frac_of_achievable"] = res["roofline"]["achieved"] / ach_read
+    tr = read_trace()
+    if tr:
+        # the same kernel's duration in the committed rocprofv3 trace of this
+        # benchmark (same source): a second clock for the same quantity
+        res["roofline"]["trace"] = {"avg_launch_us": tr[0], "achieved": alg_bytes / (tr[0] * 1e-6) / 1e9,
+                                    "frac": alg_bytes / (tr[0] * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+                                    "reduce_avg_launch_us": tr[1],
+                                    "source": os.path.relpath(TRACE_FILE, ROOT)}
     res["roofline"]["achievable_probe"] = (f"probe_read streaming one layer's W_gate "
                                            f"({stack.data['w_gate'][0].numel() * 2 / 1e6:.1f} MB) per launch, "
                                            f"{L} layers")
@@ -309,6 +359,8 @@ def run_mistral(args, ts, synth, torch):
         rel = parity_layers(ts, torch, stack, synth, (0, L - 1))
         res["parity_layer0_rel_l2"] = rel[0]
         res["parity_last_layer_rel_l2"] = rel[L - 1]
+    if not args.no_configs:
+        res["configs"] = run_configs(args, ts, synth, torch)
     res["paper_context"] = {
         "note": "context only: other hardware, whole-model decode, predictor-driven PowerInfer vs dense llama.cpp",
         "decode_speedup": "2-5x (i9-14900HX + RTX 4090 Laptop; i7-12700K + RTX 2080Ti)",
@@ -332,31 +384,70 @@ def run_probes(ts, torch):
             "copy_GBps": 2 * dst.numel() * 2 / (ms2 * 1e-3) / 1e9, "copy_bytes": dst.numel() * 2}
 
 
+SWEEP = (0.50, 0.75, 0.90, 0.95, 0.99)
+
+
+def ffn_entry(args, ts, synth, torch, workload, batch, gate_bias, seed, dtype=None, hidden=H_MISTRAL,
+              inter=I_MISTRAL, layers=None, steps=None, warmup=None, parity=True, extra=None):
+    """One FFN stack configuration, measured: tokens/s/layer and touched
+    GB/s of the sparse path, the dense comparator on the same stack, the
+    byte-bound speedup, the dominant kernels' event-pair durations, and the
+    parity of the first and last layers against the fp64 oracle."""
+    L = layers or args.layers
+    steps = steps or args.steps
+    warmup = args.warmup if warmup is None else warmup
+    stack = Stack(ts, synth, L, batch, hidden, inter, gate_bias=gate_bias, seed=seed, dtype=dtype)
+    counts = stack.counts()  # per layer (n_G, n_A); unions over the batch when batch > 1
+    H, I, B, esz = hidden, inter, batch, stack.esz
+    t_s = timed(torch, stack.step_sparse, steps, warmup)
+    t_d = None if args.no_dense else timed(torch, stack.step_dense, steps, warmup)
+    alg = sum(bytes_sparse(esz, H, I, ng, na, B) for ng, na in counts) / L
+    dense = 3 * esz * H * I + 4 * B * H
+    res = {"workload": workload, "batch": B, "hidden": H, "inter": I, "layers": L,
+           "dtype": "bf16" if stack.dtype == synth.BF16 else "f32", "steps": steps, **(extra or {}),
+           ("union_gate_fraction" if B > 1 else "gate_fraction"): sum(c[0] for c in counts) / (L * I),
+           ("union_active_fraction" if B > 1 else "active_fraction"): sum(c[1] for c in counts) / (L * I),
+           "us_per_layer": t_s / L * 1e6, "sparse_tokens_per_s_layer": B * L / t_s,
+           "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t_s / L) / 1e9,
+           "sparse_frac_touched": alg / (t_s / L) / 1e9 / HBM_PEAK_GBPS}
+    if t_d:
+        res.update({"dense_tokens_per_s_layer": B * L / t_d, "dense_GBps": dense / (t_d / L) / 1e9,
+                    "speedup_vs_dense": t_d / t_s, "byte_bound_speedup": dense / alg,
+                    "target_speedup_0.6x_byte_bound": 0.6 * dense / alg})
+    kst = max(3, steps // 2)
+    if B == 1 or stack.dtype != synth.BF16:
+        rl = roofline_main(ts, torch, stack, counts, kst)
+        res.update({"ffn_main_us": rl.get("avg_launch_us"), "ffn_main_GBps": rl.get("achieved"),
+                    "ffn_main_frac": rl.get("frac"),
+                    "ffn_reduce_us": rl.get("reduce", {}).get("avg_launch_us")})
+    else:
+        kt = batch_kernels(ts, torch, stack.step_sparse, kst)
+        res.update(kt)
+        gu = sum(esz * H * (I + ng) for ng, _ in counts) / L
+        dn = sum(esz * H * na for _, na in counts) / L
+        res["gate_up_bytes_per_layer"], res["down_bytes_per_layer"] = gu, dn
+        if kt.get("batch_gate_up_us"):
+            res["batch_gate_up_GBps"] = gu / (kt["batch_gate_up_us"] * 1e-6) / 1e9
+        if kt.get("batch_down_us"):
+            res["batch_down_GBps"] = dn / (kt["batch_down_us"] * 1e-6) / 1e9
+    if parity and not args.no_parity:
+        rel = parity_layers(ts, torch, stack, synth, (0, L - 1))
+        res["parity_layer0_rel_l2"] = rel[0]
+        res["parity_last_layer_rel_l2"] = rel[L - 1]
+    del stack
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_sweep(args, ts, synth, torch):
     """Gate bias set for 50/75/90/95/99% zero Combined activations on the
     Mistral-shaped stack, batch 1; dense comparator on every point."""
     out = []
-    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
-    for s in (0.50, 0.75, 0.90, 0.95, 0.99):
+    for s in SWEEP:
         b = synth.gate_bias_for_combined_sparsity(s)
-        stack = Stack(ts, synth, L, 1, H, I, gate_bias=b, seed=1)
-        counts = stack.counts()
-        ts_ = timed(torch, stack.step_sparse, args.steps, args.warmup)
-        td = timed(torch, stack.step_dense, args.steps, args.warmup)
-        rl = roofline_main(ts, torch, stack, counts, args.steps)
-        alg = sum(bytes_sparse(2, H, I, ng, na, 1) for ng, na in counts) / L
-        dense = 3 * 2 * H * I
-        out.append({"workload": "mistral7b_ffn_stack_bf16_b1_sweep", "target_sparsity": s, "gate_bias": b,
-                    "measured_sparsity": 1 - sum(c[1] for c in counts) / (L * I),
-                    "sparse_tokens_per_s_layer": L / ts_, "dense_tokens_per_s_layer": L / td,
-                    "speedup": td / ts_, "byte_bound_speedup": dense / alg,
-                    "target_speedup_0.6x_byte_bound": 0.6 * dense / alg,
-                    "literal_target_0.6_over_1_minus_s": 0.6 / (1 - s),
-                    "sparse_GBps_touched": alg / (ts_ / L) / 1e9, "dense_GBps": dense / (td / L) / 1e9,
-                    "ffn_main_us": rl["avg_launch_us"], "ffn_main_GBps": rl["achieved"],
-                    "ffn_reduce_us": rl["reduce"]["avg_launch_us"]})
-        del stack
-        torch.cuda.empty_cache()
+        out.append(ffn_entry(args, ts, synth, torch, f"mistral7b_ffn_stack_bf16_b1_s{round(s * 100)}", 1, b, seed=1,
+                             extra={"target_sparsity": s, "gate_bias": b,
+                                    "literal_target_0.6_over_1_minus_s": 0.6 / (1 - s)}))
     return out
 
 
@@ -513,34 +604,12 @@ def run_batch_workload(args, ts, synth, torch):
     """Mistral-shaped FFN stack with a batch of independent decode tokens
     (batch 8 and 32): literal generator (each token ~90% sparse, union grows
     with the batch) and the skewed hot/cold variant (union ~67% sparse)."""
-    import numpy as np
     out = []
-    H, I, L = H_MISTRAL, I_MISTRAL, args.layers
     for B in (int(b) for b in args.batch_sizes.split(",")):
         for variant in args.variants.split(","):
-            bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(I, seed=11)
-            stack = Stack(ts, synth, L, B, H, I, gate_bias=bias, seed=2)
-            counts = stack.counts()  # unions over the batch
-            t_s = timed(torch, stack.step_sparse, args.steps, args.warmup)
-            t_d = None if args.no_dense else timed(torch, stack.step_dense, args.steps, args.warmup)
-            alg = sum(2 * H * (I + ng + na) + 8 * B * H for ng, na in counts) / L
-            # per kernel: gate+up reads W_gate whole and the union's W_up rows, down the union's W_down_t rows
-            alg_gu = sum(2 * H * (I + ng) for ng, _ in counts) / L
-            alg_dn = sum(2 * H * na for _, na in counts) / L
-            dense = 3 * 2 * H * I + 8 * B * H
-            kt = batch_kernels(ts, torch, stack.step_sparse, max(3, args.steps // 3))
-            out.append({"workload": f"mistral7b_ffn_stack_bf16_b{B}_{variant}", "batch": B, "layers": L,
-                        "union_gate_fraction": sum(c[0] for c in counts) / (L * I),
-                        "union_active_fraction": sum(c[1] for c in counts) / (L * I),
-                        "sparse_tokens_per_s_layer": B * L / t_s,
-                        "dense_tokens_per_s_layer": B * L / t_d if t_d else None,
-                        "speedup": t_d / t_s if t_d else None, "byte_bound_speedup": dense / alg,
-                        "sparse_GBps_touched": alg / (t_s / L) / 1e9,
-                        "dense_GBps": dense / (t_d / L) / 1e9 if t_d else None,
-                        "gate_up_bytes_per_layer": alg_gu, "down_bytes_per_layer": alg_dn,
-                        "us_per_layer": t_s / L * 1e6, **kt})
-            del stack
-            torch.cuda.empty_cache()
+            bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(I_MISTRAL, seed=11)
+            out.append(ffn_entry(args, ts, synth, torch, f"mistral7b_ffn_stack_bf16_b{B}_{variant}", B, bias, seed=2,
+                                 extra={"variant": variant}))
     return out
 
 
@@ -615,37 +684,107 @@ class MoEStack:
         return sp, dn
 
 
+def parity_moe_layers(ts, torch, stack, synth, layers):
+    """The sparse MoE layer's output of the given stack layers against the
+    fp64 oracle (relative L2 over the tokens whose k-th and (k+1)-th oracle
+    probabilities are not within 1e-6, relative; routing compared on them)."""
+    import numpy as np
+    import oracle
+    d, K, E = stack.d, stack.K, stack.E
+    rel, route_ok = {}, True
+    h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
+    for l in layers:
+        out, idx, _ = ts.moe_sparse(d["x"][l], d["w_router"][l], d["w_gate"][l], d["w_up"][l], d["w_down_t"][l], K)
+        torch.cuda.synchronize()
+        ref = oracle.moe(d["x"][l].cpu().numpy(), h(d["w_router"][l]), h(d["w_gate"][l]), h(d["w_up"][l]),
+                         h(d["w_down_t"][l]), synth.BF16, K, threads=oracle.max_threads(), keep_projections=False)
+        p = np.sort(ref.probs, axis=1)[:, ::-1]
+        keep = [t for t in range(stack.B) if not (K < E and abs(p[t, K - 1] - p[t, K]) <= 1e-6 * p[t, K - 1])]
+        rel[l] = _rel_l2(out.cpu().numpy()[keep], ref.y[keep])
+        route_ok = route_ok and idx.cpu().numpy()[keep].tolist() == ref.topk_idx[keep].tolist()
+    return rel, route_ok
+
+
+def moe_entry(args, ts, synth, torch, B, sp_target, bias, layers=8, steps=None, warmup=None, parity=True):
+    """Mixtral-shaped MoE layer stack (8 experts, top 2, bf16), measured as
+    ffn_entry measures the FFN."""
+    H, I, E, K, L = H_MISTRAL, I_MISTRAL, 8, 2, layers
+    steps = steps or args.steps
+    warmup = args.warmup if warmup is None else warmup
+    stack = MoEStack(ts, synth, L, B, H, I, E, K, gate_bias=bias, seed=4)
+    sp, dn = stack.touched()
+    t_s = timed(torch, stack.step_sparse, steps, warmup)
+    t_d = None if args.no_dense else timed(torch, stack.step_dense, steps, warmup)
+    alg, dense = sum(sp) / L, sum(dn) / L
+    res = {"workload": f"mixtral_moe_bf16_b{B}_s{int(sp_target * 100)}", "batch": B, "layers": L, "experts": E,
+           "top_k": K, "in_expert_sparsity_target": sp_target, "gate_bias": bias, "steps": steps,
+           "us_per_layer": t_s / L * 1e6, "sparse_tokens_per_s_layer": B * L / t_s,
+           "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t_s / L) / 1e9,
+           "sparse_frac_touched": alg / (t_s / L) / 1e9 / HBM_PEAK_GBPS}
+    if t_d:
+        res.update({"dense_tokens_per_s_layer": B * L / t_d, "dense_GBps": dense / (t_d / L) / 1e9,
+                    "speedup_vs_dense": t_d / t_s, "byte_bound_speedup": dense / alg,
+                    "target_speedup_0.6x_byte_bound": 0.6 * dense / alg})
+    kst = max(3, steps // 2)
+    if B == 1:
+        for k in ("moe_router", "ffn_main", "ffn_reduce"):
+            n, ms = kernel_avg_ms(ts, torch, stack.step_sparse, kst, k)
+            if n:
+                res[k + "_us"] = ms * 1e3
+    else:
+        res.update(batch_kernels(ts, torch, stack.step_sparse, kst))
+    if parity and not args.no_parity:
+        rel, route_ok = parity_moe_layers(ts, torch, stack, synth, (0, L - 1))
+        res["parity_layer0_rel_l2"] = rel[0]
+        res["parity_last_layer_rel_l2"] = rel[L - 1]
+        res["parity_routing_exact"] = route_ok
+    del stack
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_moe_workload(args, ts, synth, torch):
     """Mixtral-shaped MoE layer: 8 experts (hidden 4096, inter 14336, bf16),
     top-2 softmax router, gate bias for 97% zero Combined activations inside
-    each expert (also the paper's 85% point at batch 1), batch 1, 16, 32 and
-    64; 8 layers so a step streams several GB."""
+    each expert (also the paper's 85% point at batch 1 and 16), batch 1, 16,
+    32 and 64; 8 layers so a step streams several GB."""
     out = []
-    H, I, E, K, L = H_MISTRAL, I_MISTRAL, 8, 2, 8
     for B in (1, 16, 32, 64):
         for sp_target, bias in ((0.97, -1.5548), (0.85, -0.5244)):
-            if B > 1 and sp_target == 0.85:
+            if B > 16 and sp_target == 0.85:
                 continue
-            stack = MoEStack(ts, synth, L, B, H, I, E, K, gate_bias=bias, seed=4)
-            sp, dn = stack.touched()
-            t_s = timed(torch, stack.step_sparse, args.steps, args.warmup)
-            t_d = timed(torch, stack.step_dense, args.steps, args.warmup)
-            alg, dense = sum(sp) / L, sum(dn) / L
-            res = {"workload": f"mixtral_moe_bf16_b{B}_s{int(sp_target * 100)}", "batch": B, "layers": L,
-                   "experts": E, "top_k": K, "sparse_tokens_per_s_layer": B * L / t_s,
-                   "dense_tokens_per_s_layer": B * L / t_d, "speedup": t_d / t_s, "byte_bound_speedup": dense / alg,
-                   "touched_bytes_per_layer": alg, "sparse_GBps_touched": alg / (t_s / L) / 1e9,
-                   "dense_GBps": dense / (t_d / L) / 1e9, "us_per_layer": t_s / L * 1e6}
-            if B == 1:
-                for k in ("moe_router", "ffn_main", "ffn_reduce"):
-                    n, ms = kernel_avg_ms(ts, torch, stack.step_sparse, max(3, args.steps // 3), k)
-                    res[k + "_us"] = ms * 1e3
-            else:
-                res.update(batch_kernels(ts, torch, stack.step_sparse, max(3, args.steps // 3)))
-            out.append(res)
-            del stack
-            torch.cuda.empty_cache()
+            out.append(moe_entry(args, ts, synth, torch, B, sp_target, bias))
     return out
+
+
+def run_configs(args, ts, synth, torch):
+    """Every workload configuration besides the headline one, shorter runs
+    (args.config_steps timed steps each), keyed by configuration:
+    the small fp32 layer (256 copies, so a step streams from HBM), batch 8
+    and 32 (independent tokens and the hot/cold variant), the MoE layer at
+    batch 1 (97% and 85% in-expert sparsity) and 16, and the sparsity sweep."""
+    st, wu = args.config_steps, args.config_warmup
+    c = {}
+    c["config0_f32_h512_i1792_b1"] = ffn_entry(
+        args, ts, synth, torch, "small_ffn_f32_h512_i1792_b1_x256", 1, -0.84, seed=0, dtype=synth.F32, hidden=512,
+        inter=1792, layers=256, steps=st, warmup=wu,
+        extra={"note": "256 independent copies of the layer so every step streams from HBM"})
+    for B in (8, 32):
+        for variant in ("independent", "hot_cold"):
+            bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(I_MISTRAL, seed=11)
+            c[f"config2_b{B}_{variant}"] = ffn_entry(
+                args, ts, synth, torch, f"mistral7b_ffn_stack_bf16_b{B}_{variant}", B, bias, seed=2, steps=st,
+                warmup=wu, extra={"variant": variant})
+    for B, sp_target, bias in ((1, 0.97, -1.5548), (1, 0.85, -0.5244), (16, 0.97, -1.5548), (16, 0.85, -0.5244)):
+        c[f"config3_moe_b{B}_s{int(sp_target * 100)}"] = moe_entry(args, ts, synth, torch, B, sp_target, bias,
+                                                                    steps=st, warmup=wu)
+    for s in SWEEP:
+        b = synth.gate_bias_for_combined_sparsity(s)
+        c[f"config4_s{round(s * 100)}"] = ffn_entry(
+            args, ts, synth, torch, f"mistral7b_ffn_stack_bf16_b1_s{round(s * 100)}", 1, b, seed=1, steps=st,
+            warmup=wu, extra={"target_sparsity": s, "gate_bias": b,
+                              "literal_target_0.6_over_1_minus_s": 0.6 / (1 - s)})
+    return c
 
 
 def main():

@@ -999,8 +999,9 @@ __global__ __launch_bounds__(kGateThreads) void ffn_gate_up(GateArgs a) {
 // [ntiles][tile] lists (padding: index -1; each tile's list ascending, the
 // tiles contiguous or interleaved):
 //   1. one batch of loads; the entries are compacted into LDS (one block
-//      scan) as key = (fp32 bits of the value) + 1 (order-preserving for
-//      non-negative floats, never 0), position and neuron index, and the
+//      scan) as key = sel_key(fp32 bits) (magnitude order, never 0; the
+//      listed dReLU Combined values are positive, so the magnitude is the
+//      value carried on), position and neuron index, and the
 //      first radix histogram is counted from registers;
 //   2. the k-th largest key by radix select over 8-bit digits, k =
 //      min(keep, entries) (histograms by LDS atomics: counts do not depend
@@ -1051,13 +1052,10 @@ __device__ __forceinline__ int sel_block_scan(int v, int *s_w, int *sum) {
     return before + inc - v;
 }
 
-// Radix digits of the selection keys (fp32 bits of non-negative values, so
-// bit 31 is 0): 8 bits from bit 23 up, the first being the exponent (one bin
-// per octave: the values crowd fewer bins with the sign bit's digit, and
-// that measured 0.3 us slower), then bits 22..15, 14..7 and 7..0, whose bit 7
-// the prefix already fixes (the bin's digit ORs in the same bit).
-constexpr int kSelTopShift = 23;
-__device__ __forceinline__ int sel_next_shift(int shift) { return shift >= 8 ? shift - 8 : (shift > 0 ? 0 : -1); }
+// Radix digits of the selection keys (sel_key / sel_mag, kSelTopShift and
+// sel_next_shift in ts_plan.h): the first digit is the exponent, one bin per
+// octave (a first digit from bit 24, the sign bit's, crowded the values into
+// fewer bins and measured 0.3 us slower).
 
 // One radix step, run by wave 0: in the 256-bin histogram, the bin holding
 // the rem-th largest counted key (1 <= rem <= keys counted).  st[0] gains
@@ -1148,12 +1146,12 @@ __global__ __launch_bounds__(kSelThreads) void ffn_topk_select(SelArgs a) {
         for (int u = 0; u < kSelPer; ++u) {
             const int e = tid + kSelThreads * u;
             if (e < span && (int32_t)ai[u] >= 0) {
-                const uint32_t key = h[u] + 1u;
+                const uint32_t key = sel_key(h[u]);  // bit 31 clear: the first digit is < 256
                 s_c[base] = key;
                 s_cp[base] = (uint16_t)e;
                 s_ci[base] = (uint16_t)ai[u];
                 ++base;
-                atomicAdd(&s_hist[(key >> kSelTopShift) & 255u], 1u);
+                atomicAdd(&s_hist[key >> kSelTopShift], 1u);
             }
         }
 #pragma unroll
@@ -1394,7 +1392,7 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
         const int c = s_tc[t], b4 = t * a.tile / 4;
         for (int q0 = 0; q0 < c; q0 += 4) {
             const u32x4 v = s_key4[b4 + q0 / 4];
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            const uint32_t w[4] = {sel_mag(v.x), sel_mag(v.y), sel_mag(v.z), sel_mag(v.w)};
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 if (q0 + i < c) f(q0 + i, w[i]);
@@ -1439,8 +1437,8 @@ __global__ __launch_bounds__(kDownThreads) void ffn_topk_down(TopkDownArgs ta) {
     }
     __syncthreads();
 
-    // 1. k = min(keep, listed entries); the k-th largest key (fp32 bits of a
-    //    non-negative value order like the value)
+    // 1. k = min(keep, listed entries); the k-th largest key (for_entries
+    //    hands out sel_mag of the fp32 bits: magnitude order, bit 31 clear)
     int mine = 0;
     for (int t = tid; t < a.ntiles; t += kDownThreads) mine += s_tc[t];
     int n;

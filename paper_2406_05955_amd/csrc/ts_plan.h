@@ -30,6 +30,22 @@ constexpr int kSelMaxTiles = 2048;        // gate+up tiles per slot the selectio
 constexpr int kSelSpan = kSelMax + 128;   // padded list positions per slot it holds (last tile's padding)
 constexpr int kIlvMaxInter = 131072;     // interleaved tiles: the activity report's LDS bitmaps hold this many neurons
 
+// Selection keys of the top-k magnitude mask (Eq. mask: the largest
+// |Combined| are kept).  A key is the fp32 bit pattern of the magnitude:
+// the sign bit cleared and NaN patterns clamped to +inf, so bit 31 is always
+// 0 and unsigned key order is magnitude order.  The selection kernel adds
+// one (sel_key) so that no listed entry has key 0.  Radix digits are 8 bits
+// from bit 23 up (the exponent first), then bits 22..15, 14..7 and 7..0;
+// the last digit repeats bit 7, which the prefix already fixes.  The
+// functions are constexpr so the kernels and the host-side checks share one
+// definition.
+constexpr uint32_t sel_mag(uint32_t bits) {
+    return (bits & 0x7fffffffu) > 0x7f800000u ? 0x7f800000u : (bits & 0x7fffffffu);
+}
+constexpr uint32_t sel_key(uint32_t bits) { return sel_mag(bits) + 1u; }
+constexpr int kSelTopShift = 23;
+constexpr int sel_next_shift(int shift) { return shift >= 8 ? shift - 8 : (shift > 0 ? 0 : -1); }
+
 // Workspace layout and launch shape shared by the single-token path (one
 // "slot" = one (token, expert) pair processed against one weight set).
 struct SlotPlan {

@@ -54,3 +54,47 @@ def test_algorithmic_bytes():
     H, I, ng, na = 4096, 14336, 2867, 1433
     assert b.bytes_sparse(2, H, I, ng, na, 1) == 2 * H * I + 2 * H * ng + 2 * H * na + 4 * H
     assert b.bytes_sparse(4, 8, 10, 0, 0, 3) == 4 * 8 * 10 + 4 * 3 * 8
+
+
+def test_trace_summary_is_used_only_for_the_source_it_was_taken_on(tmp_path, monkeypatch):
+    b = load_bench()
+    f = tmp_path / "trace.txt"
+    monkeypatch.setattr(b, "TRACE_FILE", str(f))
+    assert b.read_trace() is None
+    f.write_text(f"kernel_source_sha256_16: {b.kernel_hash()}\nffn_main_avg_us: 27.25\nffn_reduce_avg_us: 4.15\n")
+    assert b.read_trace() == (27.25, 4.15)
+    f.write_text("kernel_source_sha256_16: 0123456789abcdef\nffn_main_avg_us: 27.25\nffn_reduce_avg_us: 4.15\n")
+    assert b.read_trace() is None
+
+
+def test_roofline_without_main_kernel_launches():
+    """A kernel sequence without ffn_main launches (tuning knobs, rows too
+    wide for the pipelined kernel) reports a null roofline instead of
+    dividing by zero."""
+    b = load_bench()
+
+    class FakeTS:
+        def prof_reset(self):
+            pass
+
+        def prof_enable(self, on):
+            pass
+
+        def prof_read(self, kernel):
+            return 0, 0.0
+
+    class FakeTorch:
+        class cuda:
+            @staticmethod
+            def synchronize():
+                pass
+
+    class FakeStack:
+        H, I, B, L, esz = 4096, 14336, 1, 2, 2
+
+        def step_sparse(self):
+            pass
+
+    rl = b.roofline_main(FakeTS(), FakeTorch(), FakeStack(), [(2867, 1433), (2867, 1433)], 3)
+    assert rl["achieved"] is None and rl["frac"] is None and rl["launches"] == 0
+    assert rl["algorithmic_bytes_per_launch"] == b.bytes_sparse(2, 4096, 14336, 2867, 1433, 1)

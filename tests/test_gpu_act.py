@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import compare_sets, ffn_inputs_to_dev, list_of, rel_l2
+from gpu_util import check_ffn_output, compare_sets, ffn_inputs_to_dev, list_of, rel_l2
 from paper_2406_05955_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -27,6 +27,8 @@ def check(inp, tau):
     torch.cuda.synchronize()
     err = rel_l2(out.cpu().numpy(), ref.y)
     assert err <= (1e-5 if inp.dtype == synth.F32 else 1e-2), (B, H, I, tau, err)
+    check_ffn_output(out.cpu().numpy(), ref.y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u, act=1,
+                     tau=tau, what=f"act B={B} H={H} I={I} tau={tau}")
     thr = 1e-6 if inp.dtype == synth.F32 else 1e-4
     for t in range(B):
         keep = np.abs(ref.g[t] - tau) >= thr

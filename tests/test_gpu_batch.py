@@ -5,13 +5,16 @@ single-token path (forced with the batch_path knob).
 Tolerance: relative L2 <= 1e-2 (bf16 weights, fp32 accumulation).  The
 batched path splits x and Combined into bf16 high / low parts, so its gate
 and up values carry about 2^-16 relative error per term; sets are compared
-outside |gate|, |up| < 1e-3."""
+outside |gate|, |up| < 1e-3.  Beside the stated tolerance every output is
+held to the path's own accuracy: relative L2 <= 1e-4 and every element
+within its worst-case rounding bound (gpu_util)."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_util import DEV, compare_sets, ffn_inputs_to_dev, list_of, rel_l2, to_dev
+from gpu_util import (DEV, TIGHT_BATCH, assert_elementwise, check_ffn_output, compare_sets, ffn_inputs_to_dev,
+                      list_of, moe_bound, rel_l2, to_dev)
 from paper_2406_05955_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -29,6 +32,8 @@ def check_batch(inp, ref=None, union=True):
     torch.cuda.synchronize()
     err = rel_l2(out.cpu().numpy(), ref.y)
     assert err <= 1e-2, (B, H, I, err)
+    check_ffn_output(out.cpu().numpy(), ref.y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u,
+                     batched=True, what=f"batch B={B} H={H} I={I}")
     for t in range(B):
         g, u = ref.g[t], ref.u[t]
         keep_g = np.abs(g) >= THR
@@ -64,7 +69,7 @@ def test_batch_matches_single_token_path():
     finally:
         ts.tune_set("batch_path", 0)
     torch.cuda.synchronize()
-    assert rel_l2(a.cpu().numpy(), b.cpu().numpy().astype(np.float64)) <= 1e-3
+    assert rel_l2(a.cpu().numpy(), b.cpu().numpy().astype(np.float64)) <= 1e-4
 
 
 def test_batch_hot_cold_union():
@@ -113,7 +118,12 @@ def moe_check(m):
     ties = [K < E and abs(p[t, K - 1] - p[t, K]) <= 1e-6 * p[t, K - 1] for t in range(B)]
     keep = [t for t in range(B) if not ties[t]]
     assert idx.cpu().numpy()[keep].tolist() == ref.topk_idx[keep].tolist()
-    assert rel_l2(out.cpu().numpy()[keep], ref.y[keep]) <= 1e-2
+    o = out.cpu().numpy()
+    assert rel_l2(o[keep], ref.y[keep]) <= 1e-2
+    assert rel_l2(o[keep], ref.y[keep]) <= TIGHT_BATCH
+    bound = moe_bound(m.x, m.w_router, m.w_gate, m.w_up, m.w_down_t, ref.topk_idx, ref.topk_w, ref.g, ref.u,
+                      batched=True, tokens=keep)
+    assert_elementwise(o[keep], ref.y[keep], bound[keep], f"moe batch B={B} H={H} I={I} E={E} K={K}")
     for t in keep:
         for k in range(K):
             s = t * K + k
@@ -152,12 +162,17 @@ def test_moe_batch_overflow_groups():
     assert rel_l2(out.cpu().numpy(), out1.cpu().numpy()) <= 1e-5
 
 
-@pytest.mark.parametrize("B", [16, 32, 64])
-def test_moe_batch_mixtral_shape(B):
-    L = synth.make_moe_stack_torch(1, B, 4096, 14336, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=3,
+@pytest.mark.parametrize("B,gate_bias", [(16, -1.5548), (32, -1.5548), (64, -1.5548), (16, -0.5244)])
+def test_moe_batch_mixtral_shape(B, gate_bias):
+    """Mixtral shape (8 experts, hidden 4096, inter 14336, bf16) at 97%
+    in-expert sparsity (b = -1.5548) and at the paper's 85% (b = -0.5244)."""
+    L = synth.make_moe_stack_torch(1, B, 4096, 14336, 8, 2, gate_bias=gate_bias, dtype=synth.BF16, seed=3,
                                    device=DEV)
     h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
     m = synth.MoEInputs(x=L["x"][0].cpu().numpy(), w_router=h(L["w_router"][0]), w_gate=h(L["w_gate"][0]),
                         w_up=h(L["w_up"][0]), w_down_t=h(L["w_down_t"][0]), dtype=synth.BF16, top_k=2,
-                        gate_bias=-1.5548)
-    moe_check(m)
+                        gate_bias=gate_bias)
+    ref, out = moe_check(m)
+    frac = 1.0 - ((ref.g > 0) & (ref.u > 0)).mean()
+    want = 0.97 if gate_bias < -1 else 0.85
+    assert abs(frac - want) < 0.01, frac

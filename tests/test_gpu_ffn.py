@@ -3,7 +3,12 @@ through the C ABI) against the fp64 oracle on seeded inputs.
 
 Tolerances (from the workload definition): relative L2 error of the output
 <= 1e-5 with fp32 weights and <= 1e-2 with bf16 weights (fp32 accumulation
-in both).  Active sets: with fp32 weights, G and A must match the oracle
+in both).  Beside them every output is held to the kernels' own accuracy:
+relative L2 <= 1e-5 on the single-token kernels (bf16 weights included: the
+weights are exact, only the fp32 accumulation differs) and <= 1e-4 on the
+matrix-core path, and every element within its worst-case rounding bound
+(gpu_util.check_ffn_output), so a single wrong element or a dropped row
+fails.  Active sets: with fp32 weights, G and A must match the oracle
 exactly on every neuron with |gate| >= 1e-6 (and |up| >= 1e-6 for A); with
 bf16 weights the kernel still reads the exact bf16 values the oracle uses,
 so the only difference is fp32 vs fp64 rounding of a 4096-term dot product
@@ -14,7 +19,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import DEV, compare_sets, ffn_inputs_to_dev, list_of, rel_l2, to_dev
+from gpu_util import DEV, check_ffn_output, compare_sets, ffn_inputs_to_dev, list_of, rel_l2, to_dev
 from paper_2406_05955_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -38,6 +43,9 @@ def check_ffn(inp, ref=None, sets=True):
     torch.cuda.synchronize()
     err = rel_l2(out.cpu().numpy(), ref.y)
     assert err <= tol_for(inp.dtype), (B, H, I, err)
+    # several bf16 tokens may take the matrix-core path (its looser bound)
+    check_ffn_output(out.cpu().numpy(), ref.y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u,
+                     batched=B > 1 and inp.dtype == synth.BF16, what=f"ffn B={B} H={H} I={I}")
     thr = set_thresh(inp.dtype)
     for t in range(B):
         g, u = ref.g[t], ref.u[t]
@@ -112,6 +120,29 @@ def test_mistral_shape_layer_full():
         assert 0.87 < frac < 0.93, frac
 
 
+def _device_layer(gate_bias, seed, B=1):
+    L = synth.make_ffn_stack_torch(1, B, 4096, 14336, gate_bias=gate_bias, dtype=synth.BF16, seed=seed, device=DEV)
+    h = lambda t: synth.tensor_to_host_array(t, synth.BF16)  # noqa: E731
+    return synth.FFNInputs(x=L["x"][0].cpu().numpy(), w_gate=h(L["w_gate"][0]), w_up=h(L["w_up"][0]),
+                           w_down_t=h(L["w_down_t"][0]), dtype=synth.BF16, gate_bias=gate_bias)
+
+
+@pytest.mark.parametrize("sparsity,gate_bias", [(0.50, 8.0), (0.75, 0.0), (0.95, -1.2816), (0.99, -2.0537)])
+def test_mistral_shape_sweep_points(sparsity, gate_bias):
+    """The sparsity sweep's other points at the full shape (hidden 4096,
+    inter 14336, bf16, batch 1), drawn on the device like the benchmark's
+    layers: at 50% every W_up row is read and about 32 active rows fall in
+    each 64-neuron tile (two rounds of the down loop); at 99% most tiles
+    hold 0-2 active rows.  Output, G and A against the oracle."""
+    inp = _device_layer(gate_bias, seed=11)
+    out, st, ref = check_ffn(inp)
+    frac = 1.0 - float(ref.n_active[0]) / 14336
+    assert abs(frac - sparsity) < 0.02, frac
+    if sparsity == 0.50:
+        assert int(ref.n_gate[0]) == 14336  # every gate open
+        assert int(st["n_gate"][0]) == 14336
+
+
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 def test_dense_comparator(dtype):
     inp = synth.make_ffn(2, 1024, 3000, gate_bias=-0.84, dtype=dtype, seed=6)
@@ -122,6 +153,9 @@ def test_dense_comparator(dtype):
     torch.cuda.synchronize()
     assert rel_l2(out_d.cpu().numpy(), ref.y) <= tol_for(dtype)
     assert rel_l2(out_d.cpu().numpy(), out_s.cpu().numpy().astype(np.float64)) <= tol_for(dtype)
+    for o, batched in ((out_d, False), (out_s, dtype == synth.BF16)):
+        check_ffn_output(o.cpu().numpy(), ref.y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u,
+                         batched=batched, what="dense comparator")
 
 
 def test_deterministic_and_workspace_canaries():
@@ -149,10 +183,15 @@ def test_batch_union_counts():
     out, st = ts.ffn_sparse(x, wg, wu, wd, union=True)
     torch.cuda.synchronize()
     assert rel_l2(out.cpu().numpy(), ref.y) <= 1e-2
+    check_ffn_output(out.cpu().numpy(), ref.y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u,
+                     batched=True, what="union counts")
     ug = int((ref.g > 0).any(axis=0).sum())
     ua = int(((ref.g > 0) & (ref.u > 0)).any(axis=0).sum())
+    # a neuron may enter or leave a union only through a token whose gate or
+    # up projection lies within the matrix-core path's rounding (1e-3)
+    near = int(((np.abs(ref.g) < 1e-3) | (np.abs(ref.u) < 1e-3)).any(axis=0).sum())
     got = st["n_union"].cpu().tolist()
-    assert abs(got[0] - ug) <= 2 and abs(got[1] - ua) <= 2, (got, ug, ua)
+    assert abs(got[0] - ug) <= near and abs(got[1] - ua) <= near, (got, ug, ua, near)
 
 
 def test_error_leaves_output_untouched():

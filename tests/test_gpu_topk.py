@@ -15,7 +15,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import compare_sets, ffn_inputs_to_dev, list_of, rel_l2
+from gpu_util import check_ffn_output, compare_sets, ffn_inputs_to_dev, list_of, rel_l2
 from paper_2406_05955_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -64,6 +64,9 @@ def check(inp, frac):
     assert torch.equal(out.view(torch.int32), fast.view(torch.int32))
     err = rel_l2(out.cpu().numpy(), y)
     assert err <= (1e-5 if inp.dtype == synth.F32 else 1e-2), (B, H, I, keep, err)
+    mult = np.stack([kept_mask(combined(ref, t), keep) for t in range(B)]).astype(np.float64)
+    check_ffn_output(out.cpu().numpy(), y, inp.x, inp.w_gate, inp.w_up, inp.w_down_t, ref.g, ref.u, mult=mult,
+                     what=f"topk B={B} H={H} I={I} keep={keep}")
     thr = 1e-6 if inp.dtype == synth.F32 else 1e-4
     for t in range(B):
         c = combined(ref, t)
@@ -152,6 +155,7 @@ def test_topk_ties_take_lower_index():
         got = set(list_of(st, "active_idx", 0, "n_active").tolist())
         assert set(trio[:take]) <= got and not (set(trio[take:]) & got), (take, trio)
         assert rel_l2(out.cpu().numpy(), y) <= 1e-2
+        assert rel_l2(out.cpu().numpy(), y) <= 1e-5  # exact bf16 weights, fp32 accumulation
         assert int(st["n_active"][0]) == int(nk[0]) == keep
 
 
@@ -195,6 +199,7 @@ def test_topk_token_with_no_open_gate():
     assert not o[1].any()
     assert int(st["n_gate"][1]) == 0 and int(st["n_active"][1]) == 0
     assert rel_l2(o[0], y[0]) <= 1e-2
+    assert rel_l2(o[0], y[0]) <= 1e-5
     assert int(st["n_active"][0]) == int(nk[0]) == keep
 
 
@@ -220,5 +225,6 @@ def test_topk_mistral_batch64():
             continue  # no clear cut on this token: GPU and oracle may keep different neurons
         assert int(st["n_active"][t]) == int(nk[t]), t
         assert rel_l2(o[t], y[t]) <= 1e-2, t
+        assert rel_l2(o[t], y[t]) <= 1e-5, t
         checked += 1
     assert checked >= 48
