@@ -226,6 +226,28 @@ ts_status ts_moe_sparse(const float *x, const void *w_router, const void *w_gate
                         int n_experts, int top_k, float *out, int32_t *topk_idx, float *topk_w,
                         const ts_ffn_stats *stats, void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * ts_ffn_sparse without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Arguments, results and errors
+ * as ts_ffn_sparse (the same kernels run); the scratch memory is a fixed
+ * array of TS_NOALLOC_SCRATCH_BYTES (32 MiB) inside the library, one per
+ * GPU, which each GPU the library runs on holds until the process ends.
+ * The first call on a device looks up that device's array (no allocation);
+ * the device current on the calling thread must be the one holding the
+ * pointers and the stream.  Shapes whose workspace (ts_ffn_workspace_bytes)
+ * exceeds the array are rejected with TS_ERR_WORKSPACE before anything is
+ * enqueued (at hidden 4096, inter 14336, bf16: batch <= 4 fits).
+ * Every call on one GPU uses the same array: calls that overlap in time on
+ * one GPU (several streams, several host threads) race and give undefined
+ * results; serialise them.  No state carries over between calls: each
+ * call writes all the scratch it reads.
+ */
+#define TS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+ts_status ts_ffn_sparse_noalloc(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                                ts_dtype wdtype, int batch, int hidden, int inter, float *out,
+                                const ts_ffn_stats *stats, void *stream);
+
 /* Dense comparator of ts_moe_sparse: same routing, every routed expert
  * computed densely.  Same arguments without the stats report. */
 ts_status ts_moe_dense(const float *x, const void *w_router, const void *w_gate, const void *w_up,

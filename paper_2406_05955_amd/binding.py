@@ -21,7 +21,7 @@ STATUS = {0: "TS_OK", 1: "TS_ERR_NULL", 2: "TS_ERR_SHAPE", 3: "TS_ERR_DTYPE", 4:
           5: "TS_ERR_WORKSPACE", 6: "TS_ERR_HIP", 7: "TS_ERR_UNSUPPORTED"}
 
 EXPORTED = ["ts_ffn_workspace_bytes", "ts_ffn_sparse", "ts_ffn_sparse_act", "ts_ffn_sparse_topk", "ts_ffn_dense",
-            "ts_ffn_given_workspace_bytes",
+            "ts_ffn_given_workspace_bytes", "ts_ffn_sparse_noalloc",
             "ts_ffn_sparse_given", "ts_moe_workspace_bytes", "ts_moe_sparse",
             "ts_moe_dense", "ts_status_str", "ts_last_error", "ts_version", "ts_prof_enable", "ts_prof_reset",
             "ts_prof_read", "ts_probe_read", "ts_probe_copy", "ts_tune_set"]
@@ -49,6 +49,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_ffn_workspace_bytes.restype = sz
     lib.ts_ffn_sparse.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp, sz, vp]
     lib.ts_ffn_sparse.restype = st
+    lib.ts_ffn_sparse_noalloc.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, vp]
+    lib.ts_ffn_sparse_noalloc.restype = st
     lib.ts_ffn_dense.argtypes = [vp, vp, vp, vp, i, i, i, i, vp, vp, sz, vp]
     lib.ts_ffn_dense.restype = st
     lib.ts_ffn_sparse_act.argtypes = [vp, vp, vp, vp, i, i, i, i, i, ctypes.c_float, vp, vp, vp, sz, vp]
@@ -91,7 +93,10 @@ lib = _load()
 
 def _check(code: int, where: str):
     if code != 0:
-        detail = lib.ts_last_error().decode() if code == 6 else ""
+        # the HIP message; the allocation-free entry point also explains a
+        # shape beyond its scratch array there
+        own = where == "ts_ffn_sparse_noalloc" and code in (5, 7)
+        detail = lib.ts_last_error().decode() if code == 6 or own else ""
         raise TSError(code, where, detail)
 
 
@@ -209,6 +214,31 @@ def ffn_sparse(x, w_gate, w_up, w_down_t, out=None, stats: bool = False, union: 
     code = lib.ts_ffn_sparse(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out),
                              ctypes.byref(st) if st is not None else None, _ptr(ws), _nbytes(ws), _stream(stream))
     _check(code, "ts_ffn_sparse")
+    return (out, d) if d is not None else out
+
+
+# the fixed scratch array of ts_ffn_sparse_noalloc (TS_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def ffn_sparse_noalloc(x, w_gate, w_up, w_down_t, out=None, stats: bool = False, union: bool = False,
+                       stream=None):
+    """ts_ffn_sparse_noalloc: ts_ffn_sparse with the library's fixed scratch
+    array instead of a workspace.  Pass `out` to make the call allocate
+    nothing on the Python side either.  Returns out, or (out, stats dict)."""
+    _check_tensors(x, w_gate, w_up, w_down_t, out)
+    B, H = x.shape
+    I = w_gate.shape[0]
+    dt = wdtype_of(w_gate)
+    if out is None:
+        out = torch.empty(B, H, dtype=torch.float32, device=x.device)
+    st, d = _stats_struct(B, I, x.device, stats or union)
+    if union:
+        d["n_union"] = torch.empty(2, dtype=torch.int32, device=x.device)
+        st.n_union = _ptr(d["n_union"])
+    code = lib.ts_ffn_sparse_noalloc(_ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(w_down_t), dt, B, H, I, _ptr(out),
+                                     ctypes.byref(st) if st is not None else None, _stream(stream))
+    _check(code, "ts_ffn_sparse_noalloc")
     return (out, d) if d is not None else out
 
 

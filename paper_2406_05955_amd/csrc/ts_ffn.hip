@@ -41,6 +41,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
+#include <mutex>
 
 #include "ts_batch.h"
 #include "ts_device.h"
@@ -2306,9 +2308,74 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free entry point (ts_ffn_sparse_noalloc): the
+// workspace of ts_ffn_sparse as a fixed array in the library's own device
+// memory, one copy per GPU.  In host code `scratch` names a host-side
+// stand-in, not a device address: the address each GPU's copy has is looked
+// up once per device (hipGetSymbolAddress, with that device current) and
+// only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[TS_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kScratchDevices] = {};
+
+// The current device's copy of `scratch` (looked up on its first use).
+ts_status scratch_on_current_device(void **ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_last_error("hipGetDevice", e);
+        return TS_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kScratchDevices) {
+        set_last_message("ts_ffn_sparse_noalloc: device index beyond the library's scratch table (64)");
+        return TS_ERR_UNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            set_last_error("hipGetSymbolAddress(scratch)", e);
+            return TS_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return TS_OK;
+}
+
 }  // namespace ts
 
 extern "C" {
+
+ts_status ts_ffn_sparse_noalloc(const float *x, const void *w_gate, const void *w_up, const void *w_down_t,
+                                ts_dtype wdtype, int batch, int hidden, int inter, float *out,
+                                const ts_ffn_stats *stats, void *stream) {
+    // every host-side check of ts_ffn_sparse first (a placeholder workspace
+    // address of the right size and alignment stands in for the scratch)
+    const size_t need = ts::ffn_ws_bytes(batch, hidden, inter, wdtype);
+    ts::SlotPlan p;
+    ts_status s = ts::check_ffn_args(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats,
+                                     reinterpret_cast<const void *>(uintptr_t{256}), need, &p);
+    if (s != TS_OK) return s;
+    if (need > TS_NOALLOC_SCRATCH_BYTES) {
+        char msg[200];
+        std::snprintf(msg, sizeof msg,
+                      "ts_ffn_sparse_noalloc: this shape needs %zu bytes of scratch, the library holds %zu",
+                      need, (size_t)TS_NOALLOC_SCRATCH_BYTES);
+        ts::set_last_message(msg);
+        return TS_ERR_WORKSPACE;
+    }
+    void *ws = nullptr;
+    s = ts::scratch_on_current_device(&ws);
+    if (s != TS_OK) return s;
+    return ts_ffn_sparse(x, w_gate, w_up, w_down_t, wdtype, batch, hidden, inter, out, stats, ws, need, stream);
+}
+
 
 ts_status ts_ffn_sparse(const float *x, const void *w_gate, const void *w_up, const void *w_down_t, ts_dtype wdtype,
                         int batch, int hidden, int inter, float *out, const ts_ffn_stats *stats, void *ws,

@@ -48,6 +48,8 @@ void set_last_error(const char *where, hipError_t e) {
     std::snprintf(g_last_error, sizeof g_last_error, "%s: %s", where, hipGetErrorString(e));
 }
 
+void set_last_message(const char *msg) { std::snprintf(g_last_error, sizeof g_last_error, "%s", msg); }
+
 ts_status check_launch(const char *where) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) {

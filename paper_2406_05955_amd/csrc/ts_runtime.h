@@ -12,6 +12,9 @@ namespace ts {
 // Stores the message of a failed HIP call for ts_last_error().
 void set_last_error(const char *where, hipError_t e);
 
+// Stores a message of the library's own for ts_last_error().
+void set_last_message(const char *msg);
+
 // Returns TS_ERR_HIP (after recording the message) if a launch failed.
 ts_status check_launch(const char *where);
 

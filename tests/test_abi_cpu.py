@@ -194,3 +194,18 @@ def test_c_program_links_the_library_only():
     assert "libturbosparse.so" in deps and "not found" not in deps.split("libturbosparse.so")[1].split("\n")[0]
     assert "amdhip64" in deps
     assert "torch" not in deps and "python" not in deps
+
+
+def test_noalloc_host_checks():
+    """ts_ffn_sparse_noalloc runs ts_ffn_sparse's checks, then rejects a
+    shape whose workspace exceeds its fixed scratch array, all before any
+    HIP call (so these return on a machine without a GPU too)."""
+    f = ts.lib.ts_ffn_sparse_noalloc
+    assert f(A, A, A, A, 1, 8, 4096, 14336, A, None, None) == WS       # ~33 MiB > 32 MiB
+    assert f(A, A, A, A, 1, 256, 4096, 14336, A, None, None) == WS
+    assert f(A, A, A, A, 1, 0, 4096, 14336, A, None, None) == SHAPE
+    assert f(None, A, A, A, 1, 1, 4096, 14336, A, None, None) == NULL
+    assert f(A + 4, A, A, A, 1, 1, 4096, 14336, A, None, None) == ALIGN
+    assert f(A, A, A, A, 7, 1, 4096, 14336, A, None, None) == DTYPE
+    assert ts.ffn_workspace_bytes(4, 4096, 14336, 1) <= ts.NOALLOC_SCRATCH_BYTES
+    assert ts.ffn_workspace_bytes(8, 4096, 14336, 1) > ts.NOALLOC_SCRATCH_BYTES
