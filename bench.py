@@ -68,6 +68,7 @@ def parse_args():
     ap.add_argument("--config-warmup", type=int, default=3, help="warm-up steps of each other configuration")
     ap.add_argument("--batch-sizes", default="8,32", help="batch workload: batch sizes")
     ap.add_argument("--variants", default="independent,hot_cold", help="batch workload: token generators")
+    ap.add_argument("--moe-batches", default="1,16,32,64", help="moe workload: batch sizes")
     return ap.parse_args()
 
 
@@ -749,7 +750,7 @@ def run_moe_workload(args, ts, synth, torch):
     each expert (also the paper's 85% point at batch 1 and 16), batch 1, 16,
     32 and 64; 8 layers so a step streams several GB."""
     out = []
-    for B in (1, 16, 32, 64):
+    for B in (int(b) for b in args.moe_batches.split(",")):
         for sp_target, bias in ((0.97, -1.5548), (0.85, -0.5244)):
             if B > 16 and sp_target == 0.85:
                 continue

@@ -38,6 +38,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "ts_batch.h"
 #include "ts_device.h"
@@ -207,6 +208,9 @@ __device__ __forceinline__ void bx_kloop(const char *wbase, const uint32_t (&rof
                                          f32x4 (&acc)[MT][Bx<TOK>::NT]) {
     using S = Bx<TOK>;
     constexpr int NX = S::NX, CPR = 4 * KS, RPI = 16 / KS, NI = MT * KS;
+    // each wave's k-steps (hpad / 128, hpad a multiple of kBxKQuant) come in
+    // batches of KS; the ring below needs their count to be a multiple of D
+    static_assert((kBxKQuant / 128 / KS) % D == 0, "k-step batches per wave must be a multiple of D");
     const int lm = lane & 15, lq = lane >> 4;
     const int lc = lane % CPR, lr = lane / CPR;
     u32x4 w[D][NI], xv[D][NX][KS];
@@ -530,6 +534,280 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
         if (lane == 0) {
             a.cnt[tix * 2] = nu;
             a.cnt[tix * 2 + 1] = na;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Gate + up over two 32-row tiles per workgroup (16 or more token slots).
+// The x fragments of a group are the largest stream the gate / up kernel
+// reads besides the weights: every workgroup reads all of them, once for the
+// gate and once for the up pass, so their L2 traffic is (workgroups) x (x
+// size) x 2.  At 32 token slots that is twice the weight bytes, and measured
+// as the kernel's limit (without the x loads the same kernel streams 5.8
+// against 3.6 TB/s).  Workgroups of 64 rows halve that traffic.  The K loop,
+// its load shapes and the accumulation order are bx_gate_up's with four
+// m-tiles instead of two, so every gate and up value is the same bits; the
+// outputs are written per 32-row tile in bx_gate_up's layout (bx_down, the
+// report and the union count read them unchanged).
+
+__device__ __forceinline__ int nth_set_bit64(uint64_t m, int n) {
+    const uint32_t lo = (uint32_t)m;
+    const int c = __popc(lo);
+    return n < c ? nth_set_bit(lo, n) : 32 + nth_set_bit((uint32_t)(m >> 32), n - c);
+}
+
+// bx_combine for MT m-tiles, two at a time through the same LDS buffer.
+template <int MT, int NT>
+__device__ __forceinline__ void bx_combine_mt(f32x4 (&acc)[MT][NT], f32x4 (*s_red)[2][NT][64], int wave, int lane) {
+#pragma unroll
+    for (int m0 = 0; m0 < MT; m0 += 2) {
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                if (m0 + mt < MT) s_red[wave][mt][nt][lane] = acc[m0 + mt][nt];
+        __syncthreads();
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                if (m0 + mt < MT)
+                    acc[m0 + mt][nt] = (s_red[0][mt][nt][lane] + s_red[1][mt][nt][lane]) +
+                                       (s_red[2][mt][nt][lane] + s_red[3][mt][nt][lane]);
+        __syncthreads();
+    }
+}
+
+// Bit j (j < 64) set where row j has pred true for some token (layout as
+// bx_any_rows, four m-tiles).
+template <int NT>
+__device__ __forceinline__ uint64_t bx_any_rows64(const bool (&pred)[4][NT][4]) {
+    uint64_t bits = 0;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint64_t m = 0;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) m |= __ballot(pred[mt][nt][i]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if ((m >> (16 * q)) & 0xFFFFull) bits |= 1ull << (16 * mt + 4 * q + i);
+        }
+    return bits;
+}
+
+// Per token (lane lm of n-tile nt) the 64-bit mask of rows with pred true,
+// rows mapped through rowbit (0..63).
+template <int NT>
+__device__ __forceinline__ void bx_token_masks64(const bool (&pred)[4][NT][4], const int (&rowbit)[4][4],
+                                                 uint64_t (&tm)[NT]) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        uint64_t m = 0;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (pred[mt][nt][i]) m |= 1ull << rowbit[mt][i];
+        uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+        lo |= (uint32_t)__shfl_xor((int)lo, 16, 64);
+        hi |= (uint32_t)__shfl_xor((int)hi, 16, 64);
+        lo |= (uint32_t)__shfl_xor((int)lo, 32, 64);
+        hi |= (uint32_t)__shfl_xor((int)hi, 32, 64);
+        tm[nt] = (uint64_t)lo | ((uint64_t)hi << 32);
+    }
+}
+
+template <int TOK, int KS, int D>
+__global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a) {
+    using S = Bx<TOK>;
+    static_assert(!S::PACK, "the 64-row kernel serves 16 or more token slots");
+    constexpr int NT = S::NT;
+    constexpr int CPR = 4 * KS, RPI = 16 / KS;
+    constexpr int RW = 2 * kBxRows;  // rows per workgroup
+    __shared__ f32x4 s_red[4][2][NT][64];
+    __shared__ float s_g[RW][TOK];
+    __shared__ __attribute__((aligned(16))) uint16_t s_h[2][kBxRows][2 * TOK];
+    __shared__ u32x4 s_stage[4][RW * CPR];  // per-wave weight staging
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lm = lane & 15, lq = lane >> 4;
+    const int ntiles2 = (a.ntiles + 1) / 2;
+    const int g = blockIdx.x / ntiles2;
+    const int t2 = blockIdx.x % ntiles2;
+    const int tile0 = 2 * t2;
+    const int nsub = min(2, a.ntiles - tile0);  // 32-row tiles this workgroup writes
+    const size_t tix0 = (size_t)g * a.ntiles + tile0;
+    const int ng = a.gcount[g];
+    if (ng == 0) {
+        if (tid < 2 * nsub) a.cnt[tix0 * 2 + tid] = 0;
+        if (a.want_masks)
+            for (int s = tid; s < nsub * TOK; s += 256) {
+                a.gmask[tix0 * TOK + s] = 0;
+                a.amask[tix0 * TOK + s] = 0;
+            }
+        return;
+    }
+    for (int e = tid; e < 2 * 2 * TOK * kBxRows / 8; e += 256)
+        reinterpret_cast<u32x4 *>(&s_h[0][0][0])[e] = u32x4{0u, 0u, 0u, 0u};
+
+    const int r0 = tile0 * kBxRows;
+    const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)(g / a.vpe) * a.expert_stride;
+    const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)(g / a.vpe) * a.expert_stride;
+    const int nks = a.hpad / 32;
+    const u32x4 *xg = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * nks * S::NX * 64;
+    const int kpw = nks / 4;  // k-steps per wave
+    const int ks0 = wave * kpw, nbat = kpw / KS;
+    u32x4 *sw = s_stage[wave];
+    const int lr = lane / CPR;
+
+    // ---- gate: 64 rows x all tokens --------------------------------------
+    f32x4 acc[4][NT];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    {
+        uint32_t roff[4 * KS];
+#pragma unroll
+        for (int j = 0; j < 4 * KS; ++j) roff[j] = 2u * (uint32_t)min(r0 + RPI * j + lr, a.I - 1) * (uint32_t)a.H;
+        bx_kloop<TOK, 4, KS, D>(reinterpret_cast<const char *>(wg), roff, a.H, xg, ks0, nbat, lane, sw, acc);
+    }
+    bx_combine_mt<4, NT>(acc, s_red, wave, lane);
+
+    bool open[4][NT][4];
+    int rowbit[4][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 16 * mt + 4 * lq + i;
+            rowbit[mt][i] = r;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                open[mt][nt][i] = r0 + r < a.I && (a.dense || acc[mt][nt][i] > 0.f);
+                if (wave == 0) s_g[r][16 * nt + lm] = acc[mt][nt][i];
+            }
+        }
+    const uint64_t umask = bx_any_rows64<NT>(open);
+    const int nu = __popcll(umask);
+    if (a.want_masks) {
+        uint64_t tm[NT];
+        bx_token_masks64<NT>(open, rowbit, tm);
+        if (wave == 0 && lq == 0)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                for (int h = 0; h < nsub; ++h)
+                    a.gmask[(tix0 + h) * TOK + 16 * nt + lm] = (uint32_t)(tm[nt] >> (32 * h));
+    }
+    __syncthreads();  // s_g complete
+
+    // ---- up: the union rows, gathered (as many m-tiles as they need) -----
+    f32x4 uacc[4][NT];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) uacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto up_pass = [&](auto mtc) {
+        constexpr int MU = decltype(mtc)::value;
+        uint32_t roff[MU * KS];
+#pragma unroll
+        for (int j = 0; j < MU * KS; ++j) {
+            const int u = RPI * j + lr;
+            roff[j] = 2u * (uint32_t)(r0 + nth_set_bit64(umask, u < nu ? u : 0)) * (uint32_t)a.H;
+        }
+        f32x4 ua[MU][NT];
+#pragma unroll
+        for (int mt = 0; mt < MU; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) ua[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        bx_kloop<TOK, MU, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, ua);
+#pragma unroll
+        for (int mt = 0; mt < MU; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) uacc[mt][nt] = ua[mt][nt];
+    };
+    if (nu > 48) up_pass(std::integral_constant<int, 4>{});
+    else if (nu > 32) up_pass(std::integral_constant<int, 3>{});
+    else if (nu > 16) up_pass(std::integral_constant<int, 2>{});
+    else if (nu > 0) up_pass(std::integral_constant<int, 1>{});
+    bx_combine_mt<4, NT>(uacc, s_red, wave, lane);
+
+    // ---- Combined for union index j = 16*mt + 4*lq + i -------------------
+    bool act[4][NT][4];
+    float hv[4][NT][4];
+    int ubit[4][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = 16 * mt + 4 * lq + i;
+            const int r = nth_set_bit64(umask, j < nu ? j : 0);
+            ubit[mt][i] = r;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const float gv = s_g[r][16 * nt + lm];
+                const float uv = uacc[mt][nt][i];
+                const bool on = j < nu && gv > 0.f && uv > 0.f;
+                act[mt][nt][i] = on || (a.dense && j < nu);
+                hv[mt][nt][i] = on ? gv * uv : 0.f;
+            }
+        }
+    const uint64_t amask_u = bx_any_rows64<NT>(act);  // over union indices
+    // union indices below nu0 are rows of the first 32-row tile
+    const int nu0 = __popc((uint32_t)umask);
+    const uint64_t below0 = nu0 >= 64 ? ~0ull : ((1ull << nu0) - 1ull);
+    const uint64_t am[2] = {amask_u & below0, amask_u & ~below0};
+    if (a.want_masks) {
+        uint64_t tm[NT];
+        bx_token_masks64<NT>(act, ubit, tm);
+        if (wave == 0 && lq == 0)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                for (int h = 0; h < nsub; ++h)
+                    a.amask[(tix0 + h) * TOK + 16 * nt + lm] = (uint32_t)(tm[nt] >> (32 * h));
+    }
+    // active union index j of tile h -> slot (its rank within the tile)
+    if (wave == 0) {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = 16 * mt + 4 * lq + i;
+                if ((amask_u >> j) & 1ull) {
+                    const int h = j < nu0 ? 0 : 1;
+                    const int slot = __popcll(am[h] & ((1ull << j) - 1ull));
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const int t = 16 * nt + lm;
+                        uint32_t hi, lo;
+                        split_hi_lo(hv[mt][nt][i], hi, lo);
+                        s_h[h][slot][t] = (uint16_t)hi;
+                        s_h[h][slot][TOK + t] = (uint16_t)lo;
+                    }
+                }
+            }
+    }
+    __syncthreads();  // s_h complete
+    for (int h = 0; h < nsub; ++h) {
+        u32x4 *hdst = reinterpret_cast<u32x4 *>(a.hfrag + (tix0 + h) * (2 * TOK * kBxRows));
+        for (int e = tid; e < 2 * TOK * kBxRows / 8; e += 256)
+            hdst[e] = reinterpret_cast<const u32x4 *>(&s_h[h][0][0])[e];
+    }
+    if (wave == 0) {
+        for (int h = 0; h < nsub; ++h) {
+            const int na = __popcll(am[h]);
+            if (lane < kBxRows) {  // an empty tile lists row 0 (always < I), never used
+                const int j = nth_set_bit64(am[h], lane < na ? lane : 0);
+                a.arow[(tix0 + h) * kBxRows + lane] =
+                    na > 0 ? (uint8_t)(nth_set_bit64(umask, j) - kBxRows * h) : (uint8_t)0;
+            }
+            if (lane == 0) {
+                a.cnt[(tix0 + h) * 2] = __popc((uint32_t)(umask >> (32 * h)));
+                a.cnt[(tix0 + h) * 2 + 1] = na;
+            }
         }
     }
 }
@@ -875,6 +1153,17 @@ T *ws_at(void *ws, size_t off) {
 template <int TOK>
 void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
     const dim3 grid((unsigned)(p.groups * p.ntiles));
+    if constexpr (TOK >= 16) {
+        // 16 or more token slots: two 32-row tiles per workgroup (half the x
+        // traffic); knob 3 keeps one tile per workgroup
+        const int knob = tuned("bx_gate");
+        if (knob != 3) {
+            const dim3 grid2((unsigned)(p.groups * ((p.ntiles + 1) / 2)));
+            // 2 k-steps per load batch (4 at 16 slots spills registers with four m-tiles)
+            launch("batch_gate_up", bx_gate_up64<TOK, 2, 2>, grid2, dim3(256), st, a);
+            return;
+        }
+    }
     if constexpr (TOK <= 16) {  // deeper shapes spill registers at 32 tokens and run slower
         switch (tuned("bx_gate")) {
         case 1: launch("batch_gate_up", bx_gate_up<TOK, 2, 2>, grid, dim3(256), st, a); return;

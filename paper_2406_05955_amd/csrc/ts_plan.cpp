@@ -385,7 +385,7 @@ ts_status ts_tune_set(const char *key, int value) {
         return TS_OK;
     }
     if (std::strcmp(key, "bx_gate") == 0) {
-        if (value < 0 || value > 2) return TS_ERR_SHAPE;
+        if (value < 0 || value > 3) return TS_ERR_SHAPE;
         ts::g_bx_gate.store(value);
         return TS_OK;
     }

@@ -176,3 +176,43 @@ def test_moe_batch_mixtral_shape(B, gate_bias):
     frac = 1.0 - ((ref.g > 0) & (ref.u > 0)).mean()
     want = 0.97 if gate_bias < -1 else 0.85
     assert abs(frac - want) < 0.01, frac
+
+
+@pytest.mark.parametrize("B,H,I,E,K", [(16, 512, 1000, 1, 1), (32, 1024, 2048, 1, 1), (64, 256, 720, 1, 1),
+                                       (20, 512, 33, 1, 1), (48, 2048, 1600, 8, 2), (64, 512, 900, 8, 2),
+                                       (40, 256, 200, 64, 8)])
+def test_gate_up_64_row_tiles_match_32_row_tiles(B, H, I, E, K):
+    """With 16 or more token slots the gate + up kernel takes two 32-row
+    tiles per workgroup; its K loop and summation order are the one-tile
+    kernel's, so the output, the report and the unions are the same bits
+    (inter odd, below 64 and not a multiple of 32 included; empty MoE groups
+    included); the dense comparator too."""
+    def run(knob):
+        ts.tune_set("bx_gate", knob)
+        try:
+            if E == 1:
+                inp = synth.make_ffn(B, H, I, gate_bias=-0.84, dtype=synth.BF16, seed=[37, B, H, I])
+                x, wg, wu, wd = ffn_inputs_to_dev(inp)
+                out, st = ts.ffn_sparse(x, wg, wu, wd, stats=True, union=True)
+                dense = ts.ffn_dense(x, wg, wu, wd)
+            else:
+                m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=synth.BF16, seed=[38, B, H, I, E, K])
+                args = [to_dev(m.x), to_dev(m.w_router), to_dev(m.w_gate), to_dev(m.w_up), to_dev(m.w_down_t)]
+                out, _, _, st = ts.moe_sparse(*args, K, stats=True)
+                dense = ts.moe_dense(*args, K)[0]
+            torch.cuda.synchronize()
+            return out.clone(), {k: v.clone() for k, v in st.items()}, dense.clone()
+        finally:
+            ts.tune_set("bx_gate", 0)
+    o64, s64, d64 = run(0)
+    o32, s32, d32 = run(3)
+    assert torch.equal(o64.view(torch.int32), o32.view(torch.int32))
+    assert torch.equal(d64.view(torch.int32), d32.view(torch.int32))
+    for k in s64:
+        if k in ("gate_idx", "active_idx"):
+            cnt = s64["n_gate" if k == "gate_idx" else "n_active"]
+            for r in range(cnt.numel()):
+                n = int(cnt[r])
+                assert torch.equal(s64[k][r, :n], s32[k][r, :n]), (k, r)
+        else:
+            assert torch.equal(s64[k], s32[k]), k
