@@ -2272,9 +2272,11 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
                                  ws, ws_bytes, &p);
     if (s != TS_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    // the routing table goes straight to the caller's arrays when given (no
+    // copies after the kernels), otherwise to the workspace
     const size_t roff = moe_route_offset(batch, hidden, inter, E, K, dt);
-    int32_t *ridx = ws_at<int32_t>(ws, roff);
-    float *rw = ws_at<float>(ws, roff + align_up256((size_t)batch * K * sizeof(int32_t)));
+    int32_t *ridx = topk_idx ? topk_idx : ws_at<int32_t>(ws, roff);
+    float *rw = topk_w ? topk_w : ws_at<float>(ws, roff + align_up256((size_t)batch * K * sizeof(int32_t)));
     BatchPlan bp;
     const size_t estride = (size_t)inter * (size_t)hidden;
     const bool batched = batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp);
@@ -2294,17 +2296,7 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
     } else {
         s = run_slots(x, wg, wu, wd, ridx, estride, dt, dense, p, out, rw, stats, ws, st);
     }
-    if (s != TS_OK) return s;
-    if (topk_idx) {
-        if (hipMemcpyAsync(topk_idx, ridx, (size_t)batch * K * sizeof(int32_t), hipMemcpyDeviceToDevice, st) !=
-            hipSuccess)
-            return check_launch("topk_idx copy");
-    }
-    if (topk_w) {
-        if (hipMemcpyAsync(topk_w, rw, (size_t)batch * K * sizeof(float), hipMemcpyDeviceToDevice, st) != hipSuccess)
-            return check_launch("topk_w copy");
-    }
-    return TS_OK;
+    return s;
 }
 
 }  // namespace
