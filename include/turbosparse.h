@@ -308,10 +308,13 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *                per group in the batched down kernel
  *   "rif"        weight rows in flight per wave in the row dot products
  *                (1 or 2)
- *   "bx_gate"    load shape of the batched gate+up kernel for up to 16
- *                tokens per group: 0 default (k-steps of 32 per batch x
- *                batches in flight: 2 x 2 for up to 8 tokens, 4 x 2 for 16),
- *                1 = 2 x 2, 2 = 2 x 4
+ *   "bx_gate"    batched gate+up kernel: 0 default (8 token slots per
+ *                group: one 32-row tile per workgroup, k-steps of 32 per
+ *                batch x batches in flight 2 x 2; 16 or more: two 32-row
+ *                tiles per workgroup, 2 x 2); for 8 slots 1 = 2 x 2,
+ *                2 = 2 x 4; for 16 slots 1 = 2 x 2 and 2 = 2 x 4 on one
+ *                tile per workgroup; 3 = one tile per workgroup with its
+ *                default load shape (4 x 2 at 16 slots, 2 x 2 past that)
  *   "bx_down"    batched down kernel for up to 32 tokens per group: 0 default
  *                (2 blocks of 32 rows in flight per wave), 1 = 3 blocks
  *   "bx_vgroup"  batched MoE layer: 0 default (token slots per expert group

@@ -1170,9 +1170,8 @@ void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
     const dim3 grid((unsigned)(p.groups * p.ntiles));
     if constexpr (TOK >= 16) {
         // 16 or more token slots: two 32-row tiles per workgroup (half the x
-        // traffic); knob 3 keeps one tile per workgroup
-        const int knob = tuned("bx_gate");
-        if (knob != 3) {
+        // traffic); knobs 1-3 keep one tile per workgroup
+        if (tuned("bx_gate") == 0) {
             const dim3 grid2((unsigned)(p.groups * ((p.ntiles + 1) / 2)));
             // 2 k-steps per load batch (4 at 16 slots spills registers with four m-tiles)
             launch("batch_gate_up", bx_gate_up64<TOK, 2, 2>, grid2, dim3(256), st, a);

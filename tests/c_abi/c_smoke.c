@@ -2,14 +2,15 @@
  * The C ABI used from plain C, without Python or PyTorch: device memory from
  * the HIP runtime, one ts_ffn_sparse call (fp32 weights, two tokens), the
  * result checked against a direct double-precision evaluation of the dReLU
- * FFN (Eq. gated-MLP with ReLU on both projections), and one argument error
- * that must leave the output untouched.  Prints "c_smoke ok" and exits 0 on
- * success.
+ * FFN (Eq. gated-MLP with ReLU on both projections), one argument error
+ * that must leave the output untouched, and the allocation-free entry point,
+ * which must give the same bits.  Prints "c_smoke ok" and exits 0 on success.
  */
 #include <hip/hip_runtime_api.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdio.h>
+#include <string.h>
 #include <stdlib.h>
 
 #include "turbosparse.h"
@@ -116,6 +117,20 @@ int main(void)
             fprintf(stderr, "output changed by a rejected call\n");
             return 1;
         }
+
+    /* the allocation-free entry point: same kernels on the library's own
+       scratch, so the same bits */
+    s = ts_ffn_sparse_noalloc(dx, dg, du, dd, TS_F32, B, H, I, dout, NULL, NULL);
+    if (s != TS_OK) {
+        fprintf(stderr, "ts_ffn_sparse_noalloc: %s (%s)\n", ts_status_str(s), ts_last_error());
+        return 1;
+    }
+    CHECK(hipDeviceSynchronize());
+    CHECK(hipMemcpy(again, dout, sizeof again, hipMemcpyDeviceToHost));
+    if (memcmp(again, out, sizeof again) != 0) {
+        fprintf(stderr, "ts_ffn_sparse_noalloc differs from ts_ffn_sparse\n");
+        return 1;
+    }
 
     hipFree(dx);
     hipFree(dg);
