@@ -82,15 +82,20 @@ def test_batch_hot_cold_union():
     assert 0.2 * 3000 < ua < 0.45 * 3000
 
 
-@pytest.mark.parametrize("B", [8, 32])
-def test_mistral_shape_batch(B):
-    """hidden 4096, inter 14336, bf16, independent tokens at 90% sparsity each,
-    drawn on the device like the benchmark's layers; every output compared."""
-    L = synth.make_ffn_stack_torch(1, B, 4096, 14336, gate_bias=-0.8416, dtype=synth.BF16, seed=7, device=DEV)
+@pytest.mark.parametrize("B,variant", [(8, "independent"), (16, "independent"), (32, "independent"),
+                                       (64, "independent"), (32, "hot_cold")])
+def test_mistral_shape_batch(B, variant):
+    """hidden 4096, inter 14336, bf16, drawn on the device like the
+    benchmark's layers: independent tokens at 90% sparsity each (8 token
+    slots: one 32-row tile per gate+up workgroup; 16, 32 and 64 slots: two
+    tiles per workgroup), and the skewed hot/cold variant at batch 32; every
+    output compared."""
+    bias = -0.8416 if variant == "independent" else synth.hot_cold_bias(14336, seed=11)
+    L = synth.make_ffn_stack_torch(1, B, 4096, 14336, gate_bias=bias, dtype=synth.BF16, seed=7, device=DEV)
     inp = synth.FFNInputs(x=L["x"][0].cpu().numpy(), w_gate=synth.tensor_to_host_array(L["w_gate"][0], synth.BF16),
                           w_up=synth.tensor_to_host_array(L["w_up"][0], synth.BF16),
                           w_down_t=synth.tensor_to_host_array(L["w_down_t"][0], synth.BF16), dtype=synth.BF16,
-                          gate_bias=-0.8416)
+                          gate_bias=bias)
     check_batch(inp)
 
 
