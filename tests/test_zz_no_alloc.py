@@ -74,3 +74,17 @@ def test_noalloc_rejects_shapes_beyond_the_scratch():
     assert torch.all(out == 7.0).item()
     # the entry point still serves a fitting shape afterwards
     _same_as_workspace_path(synth.make_ffn(3, 256, 700, gate_bias=-0.5, dtype=synth.BF16, seed=92))
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_noalloc_graph_capture(B):
+    """What the entry point is for: a call captured into a HIP graph with no
+    workspace to allocate.  The first call on the device (warm-up, outside
+    the capture) looks the scratch up; the captured call only enqueues
+    kernels.  Four replays with new inputs written between them (eager work
+    on the same stream), each equal bit for bit to an eager call."""
+    from test_gpu_graph import _ffn, replay_check
+    H, I = 1024, 2000
+    x, (wg, wu, wd), fresh = _ffn(B, H, I, 94)
+    out = torch.empty(B, H, dtype=torch.float32, device=DEV)
+    replay_check(lambda xx: ts.ffn_sparse_noalloc(xx, wg, wu, wd, out=out if xx is x else None), x, fresh)
