@@ -321,6 +321,12 @@ ts_status ts_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  *                about twice the expected expert load; an expert with more
  *                tokens takes further groups), 1 = one group per expert
  *                with slots for the whole batch
+ *   "bx_xtok"    batched MoE layer: 0 default (the router also writes
+ *                each token's x as bf16 high / low parts and the gate+up
+ *                kernel gathers its group's tokens from them: no dispatch
+ *                kernel, one copy of x for all expert groups), 1 = a
+ *                dispatch kernel builds per-group x fragments (as the
+ *                batched FFN does)
  *   "ffn_interleave" single-token kernels: 0 default (workgroup t takes
  *                neurons t, t + T, t + 2 T, ... of T workgroups per token,
  *                so the grid streams one narrow band of each matrix at a

@@ -16,7 +16,10 @@
 // accuracy; with at most 8 token slots both parts share one 16-column MFMA
 // tile (columns 0-7 high, 8-15 low) and are added at the end.  Kernels:
 //   bx_prep      routing table -> per-group token lists (MoE), and x of each
-//                group's tokens split into bf16 high and low parts
+//                group's tokens split into bf16 high and low parts (the
+//                batched FFN; in the MoE layer the router writes every
+//                token's split once, and bx_gate_up lists its group's tokens
+//                and gathers their columns itself)
 //   bx_gate_up   per 32-neuron tile, 4 waves each a quarter of the hidden
 //                dimension with its own pipelined loads (no barrier inside
 //                the K loop): gate for all tokens, union of open gates, up
@@ -56,17 +59,6 @@ __device__ __forceinline__ f32x4 mfma_bf16(const u32x4 a, const u32x4 b, const f
                                                    0, 0, 0);
 }
 
-// fp32 -> bf16 bits, round to nearest even (finite inputs).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
-
-__device__ __forceinline__ void split_hi_lo(float x, uint32_t &hi, uint32_t &lo) {
-    hi = bf16_bits(x);
-    lo = bf16_bits(x - __uint_as_float(hi << 16));
-}
-
 // Shape constants per token-slot count TOK (8, 16, 32, 64).
 template <int TOK>
 struct Bx {
@@ -100,7 +92,81 @@ struct BxArgs {
     float *out;              // [tokens][H]
     int want_masks;
     int dense;               // 1: every row is taken (the dense comparator)
+    const uint16_t *xtok;    // or null: every token's x as bf16 high / low parts, token-major (the MoE
+                             // router's split: per token xchunks chunks of 8 values, 32 bytes each)
+    int xchunks;
 };
+
+// x operand source of the gate / up K loop: the per-group fragments built by
+// bx_prep (frag), or (GATHER) this lane's columns gathered from the
+// token-major split, off[f] = the byte offset of fragment f's column at
+// k-step 0 (past the resource for an empty slot: zeros).
+template <int NX>
+struct BxX {
+    const u32x4 *frag;
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t off[NX];
+};
+
+// The gate / up kernels' x source for group g: lane (lm, lq) of fragment f
+// holds column lm = (part, slot) as bx_prep lays it out; gathered from the
+// token-major split when the router wrote one (a.xtok), each column at
+// 16 bytes of its token's 32-byte chunk 4 ks + lq (high part first).
+template <int TOK, bool GATHER>
+__device__ __forceinline__ BxX<Bx<TOK>::NX> bx_xsource(const BxArgs &a, int g, int lane, const int *s_tok) {
+    using S = Bx<TOK>;
+    constexpr int NX = S::NX;
+    const int lm = lane & 15, lq = lane >> 4;
+    BxX<NX> xs;
+    xs.frag = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * (a.hpad / 32) * NX * 64;
+    if constexpr (GATHER) {
+        const uint32_t rowb = (uint32_t)a.xchunks * 32u;
+        xs.rs = make_rsrc(a.xtok, (uint32_t)a.B * rowb);
+#pragma unroll
+        for (int f = 0; f < NX; ++f) {
+            const int hl = S::PACK ? (lm >> 3) : (f & 1);
+            const int slot = S::PACK ? (lm & 7) : 16 * (f >> 1) + lm;
+            const int tk = s_tok[slot];
+            xs.off[f] = tk >= 0 ? (uint32_t)tk * rowb + 32u * (uint32_t)lq + 16u * (uint32_t)hl : kOutOfRange;
+        }
+    } else {
+        xs.rs = make_rsrc(a.xhl, 0u);
+#pragma unroll
+        for (int f = 0; f < NX; ++f) xs.off[f] = kOutOfRange;
+    }
+    return xs;
+}
+
+// Group g's token list (MoE): the tokens routed to expert g / vpe, entries
+// [r0, r0 + TOK) of that expert's ascending list, by one wave scanning the
+// (token, rank) pairs in token-major order; s_tok[slot] = token, -1 past the
+// count.  With `tables`, also the group's token count and the (group, slot)
+// of each of its routed pairs (for the reduce and the report).  Returns the
+// count (on every lane).
+template <int TOK>
+__device__ __forceinline__ int bx_list_group(const BxArgs &a, int g, int lane, int *s_tok, bool tables) {
+    const int np = a.B * a.K;
+    const int e = g / a.vpe, r0 = (g - e * a.vpe) * TOK;
+    int base = 0;
+    for (int p0 = 0; p0 < np; p0 += 64) {
+        const int p = p0 + lane;
+        const bool mine = p < np && a.topk[p] == e;
+        const uint64_t m = __ballot(mine);
+        const int rank = base + lane_prefix(m, lane) - r0;  // rank within this group
+        if (mine && rank >= 0 && rank < TOK) {
+            s_tok[rank] = p / a.K;
+            if (tables) {
+                a.tslot[p * 2] = g;
+                a.tslot[p * 2 + 1] = rank;
+            }
+        }
+        base += __popcll(m);
+    }
+    const int n = min(max(base - r0, 0), TOK);
+    for (int sl = n + lane; sl < TOK; sl += 64) s_tok[sl] = -1;
+    if (tables && lane == 0) a.gcount[g] = n;
+    return n;
+}
 
 // ---------------------------------------------------------------------------
 // x of each group's token slots as MFMA operand fragments: for k-step ks (32
@@ -124,30 +190,7 @@ __global__ __launch_bounds__(256) void bx_prep(BxArgs a) {
     const int g = (blockIdx.x * 4) / (NX * nks);
     const bool first = blockIdx.x * 4 == g * NX * nks;
     if (a.topk) {
-        // group g holds entries [r0, r0 + TOK) of expert g / vpe's list
-        if (threadIdx.x < 64) {
-            const int lane = threadIdx.x;
-            const int np = a.B * a.K;
-            const int e = g / a.vpe, r0 = (g - e * a.vpe) * TOK;
-            int base = 0;
-            for (int p0 = 0; p0 < np; p0 += 64) {
-                const int p = p0 + lane;
-                const bool mine = p < np && a.topk[p] == e;
-                const uint64_t m = __ballot(mine);
-                const int rank = base + lane_prefix(m, lane) - r0;  // rank within this group
-                if (mine && rank >= 0 && rank < TOK) {
-                    s_tok[rank] = p / a.K;
-                    if (first) {
-                        a.tslot[p * 2] = g;
-                        a.tslot[p * 2 + 1] = rank;
-                    }
-                }
-                base += __popcll(m);
-            }
-            const int n = min(max(base - r0, 0), TOK);
-            for (int sl = n + lane; sl < TOK; sl += 64) s_tok[sl] = -1;
-            if (first && lane == 0) a.gcount[g] = n;
-        }
+        if (threadIdx.x < 64) bx_list_group<TOK>(a, g, threadIdx.x, s_tok, first);
         __syncthreads();
     } else if (blockIdx.x == 0) {
         for (int t = threadIdx.x; t < a.B; t += 256) {
@@ -202,9 +245,9 @@ __device__ __forceinline__ int bx_swz(int r, int c) {
     return KS == 4 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
 }
 
-template <int TOK, int MT, int KS, int D>
+template <int TOK, int MT, int KS, int D, bool GATHER = false>
 __device__ __forceinline__ void bx_kloop(const char *wbase, const uint32_t (&roff)[MT * KS], int H,
-                                         const u32x4 *__restrict__ xg, int ks0, int nbat, int lane, u32x4 *sw,
+                                         const BxX<Bx<TOK>::NX> &xs, int ks0, int nbat, int lane, u32x4 *sw,
                                          f32x4 (&acc)[MT][Bx<TOK>::NT]) {
     using S = Bx<TOK>;
     constexpr int NX = S::NX, CPR = 4 * KS, RPI = 16 / KS, NI = MT * KS;
@@ -221,11 +264,21 @@ __device__ __forceinline__ void bx_kloop(const char *wbase, const uint32_t (&rof
         const uint32_t kw = 2u * (uint32_t)(k < H ? k : H - 8);
 #pragma unroll
         for (int j = 0; j < NI; ++j) w[d][j] = ld_stream(wbase + (roff[j] + kw));
-        const u32x4 *xb = xg + (size_t)(ks0 + b * KS) * NX * 64;
+        if constexpr (GATHER) {
+            // 128 bytes per token and k-step: the lane's 16 (its k-range, its part)
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
+            for (int s = 0; s < KS; ++s)
 #pragma unroll
-            for (int f = 0; f < NX; ++f) xv[d][f][s] = ld_cached(xb + (s * NX + f) * 64 + lane);
+                for (int f = 0; f < NX; ++f)
+                    xv[d][f][s] = __builtin_amdgcn_raw_buffer_load_b128(
+                        xs.rs, xs.off[f] + (uint32_t)(ks0 + b * KS + s) * 128u, 0, 0);
+        } else {
+            const u32x4 *xb = xs.frag + (size_t)(ks0 + b * KS) * NX * 64;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int f = 0; f < NX; ++f) xv[d][f][s] = ld_cached(xb + (s * NX + f) * 64 + lane);
+        }
     };
     auto mma = [&](int d) {
 #pragma unroll
@@ -360,7 +413,7 @@ __device__ __forceinline__ int nth_set_bit(uint32_t m, int n) {
     return pos;
 }
 
-template <int TOK, int KS, int D>
+template <int TOK, int KS, int D, bool GATHER = false>
 __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
     using S = Bx<TOK>;
     constexpr int NT = S::NT, NX = S::NX;
@@ -369,13 +422,27 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
     __shared__ float s_g[kBxRows][TOK];
     __shared__ __attribute__((aligned(16))) uint16_t s_h[kBxRows][2 * TOK];
     __shared__ u32x4 s_stage[4][kBxRows * CPR];  // per-wave weight staging
+    __shared__ int s_tok[GATHER ? TOK : 1];
+    __shared__ int s_ng;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
     const int g = blockIdx.x / a.ntiles;
     const int tile = blockIdx.x % a.ntiles;
     const size_t tix = (size_t)g * a.ntiles + tile;
-    const int ng = a.gcount[g];
+    int ng;
+    if constexpr (GATHER) {
+        // the group's tokens from the routing table; its first tile's
+        // workgroup writes the group tables
+        if (wave == 0) {
+            const int n = bx_list_group<TOK>(a, g, lane, s_tok, tile == 0);
+            if (lane == 0) s_ng = n;
+        }
+        __syncthreads();
+        ng = s_ng;
+    } else {
+        ng = a.gcount[g];
+    }
     if (ng == 0) {
         if (tid == 0) {
             a.cnt[tix * 2] = 0;
@@ -395,7 +462,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
     const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)(g / a.vpe) * a.expert_stride;
     const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)(g / a.vpe) * a.expert_stride;
     const int nks = a.hpad / 32;
-    const u32x4 *xg = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * nks * NX * 64;
+    const BxX<NX> xs = bx_xsource<TOK, GATHER>(a, g, lane, s_tok);
     const int kpw = nks / 4;  // k-steps per wave
     const int ks0 = wave * kpw, nbat = kpw / KS;
     u32x4 *sw = s_stage[wave];
@@ -413,7 +480,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
         uint32_t roff[2 * KS];
 #pragma unroll
         for (int j = 0; j < 2 * KS; ++j) roff[j] = 2u * (uint32_t)min(r0 + RPI * j + lr, a.I - 1) * (uint32_t)a.H;
-        bx_kloop<TOK, 2, KS, D>(reinterpret_cast<const char *>(wg), roff, a.H, xg, ks0, nbat, lane, sw, acc);
+        bx_kloop<TOK, 2, KS, D, GATHER>(reinterpret_cast<const char *>(wg), roff, a.H, xs, ks0, nbat, lane, sw, acc);
     }
     bx_combine<NT>(acc, s_red, wave, lane);
     bx_pair_sum<TOK>(acc);
@@ -456,7 +523,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
             const int u = RPI * j + lr;
             roff[j] = 2u * (uint32_t)(r0 + nth_set_bit(umask, u < nu ? u : 0)) * (uint32_t)a.H;
         }
-        bx_kloop<TOK, 2, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, uacc);
+        bx_kloop<TOK, 2, KS, D, GATHER>(reinterpret_cast<const char *>(wu), roff, a.H, xs, ks0, nbat, lane, sw, uacc);
     } else if (nu > 0) {
         uint32_t roff[KS];
 #pragma unroll
@@ -467,7 +534,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up(BxArgs a) {
         f32x4 u1[1][NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) u1[0][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        bx_kloop<TOK, 1, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, u1);
+        bx_kloop<TOK, 1, KS, D, GATHER>(reinterpret_cast<const char *>(wu), roff, a.H, xs, ks0, nbat, lane, sw, u1);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) uacc[0][nt] = u1[0][nt];
     }
@@ -620,7 +687,7 @@ __device__ __forceinline__ void bx_token_masks64(const bool (&pred)[4][NT][4], c
     }
 }
 
-template <int TOK, int KS, int D>
+template <int TOK, int KS, int D, bool GATHER = false>
 __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a) {
     using S = Bx<TOK>;
     static_assert(!S::PACK, "the 64-row kernel serves 16 or more token slots");
@@ -631,6 +698,8 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
     __shared__ float s_g[RW][TOK];
     __shared__ __attribute__((aligned(16))) uint16_t s_h[2][kBxRows][2 * TOK];
     __shared__ u32x4 s_stage[4][RW * CPR];  // per-wave weight staging
+    __shared__ int s_tok[GATHER ? TOK : 1];
+    __shared__ int s_ng;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
@@ -640,7 +709,19 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
     const int tile0 = 2 * t2;
     const int nsub = min(2, a.ntiles - tile0);  // 32-row tiles this workgroup writes
     const size_t tix0 = (size_t)g * a.ntiles + tile0;
-    const int ng = a.gcount[g];
+    int ng;
+    if constexpr (GATHER) {
+        // the group's tokens from the routing table; its first workgroup
+        // writes the group tables
+        if (wave == 0) {
+            const int n = bx_list_group<TOK>(a, g, lane, s_tok, t2 == 0);
+            if (lane == 0) s_ng = n;
+        }
+        __syncthreads();
+        ng = s_ng;
+    } else {
+        ng = a.gcount[g];
+    }
     if (ng == 0) {
         if (tid < 2 * nsub) a.cnt[tix0 * 2 + tid] = 0;
         if (a.want_masks)
@@ -657,7 +738,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
     const uint16_t *wg = reinterpret_cast<const uint16_t *>(a.wg) + (size_t)(g / a.vpe) * a.expert_stride;
     const uint16_t *wu = reinterpret_cast<const uint16_t *>(a.wu) + (size_t)(g / a.vpe) * a.expert_stride;
     const int nks = a.hpad / 32;
-    const u32x4 *xg = reinterpret_cast<const u32x4 *>(a.xhl) + (size_t)g * nks * S::NX * 64;
+    const BxX<S::NX> xs = bx_xsource<TOK, GATHER>(a, g, lane, s_tok);
     const int kpw = nks / 4;  // k-steps per wave
     const int ks0 = wave * kpw, nbat = kpw / KS;
     u32x4 *sw = s_stage[wave];
@@ -673,7 +754,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
         uint32_t roff[4 * KS];
 #pragma unroll
         for (int j = 0; j < 4 * KS; ++j) roff[j] = 2u * (uint32_t)min(r0 + RPI * j + lr, a.I - 1) * (uint32_t)a.H;
-        bx_kloop<TOK, 4, KS, D>(reinterpret_cast<const char *>(wg), roff, a.H, xg, ks0, nbat, lane, sw, acc);
+        bx_kloop<TOK, 4, KS, D, GATHER>(reinterpret_cast<const char *>(wg), roff, a.H, xs, ks0, nbat, lane, sw, acc);
     }
     bx_combine_mt<4, NT>(acc, s_red, wave, lane);
 
@@ -723,7 +804,7 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
         for (int mt = 0; mt < MU; ++mt)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) ua[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        bx_kloop<TOK, MU, KS, D>(reinterpret_cast<const char *>(wu), roff, a.H, xg, ks0, nbat, lane, sw, ua);
+        bx_kloop<TOK, MU, KS, D, GATHER>(reinterpret_cast<const char *>(wu), roff, a.H, xs, ks0, nbat, lane, sw, ua);
 #pragma unroll
         for (int mt = 0; mt < MU; ++mt)
 #pragma unroll
@@ -1174,9 +1255,23 @@ void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
         if (tuned("bx_gate") == 0) {
             const dim3 grid2((unsigned)(p.groups * ((p.ntiles + 1) / 2)));
             // 2 k-steps per load batch (4 at 16 slots spills registers with four m-tiles)
-            launch("batch_gate_up", bx_gate_up64<TOK, 2, 2>, grid2, dim3(256), st, a);
+            if (a.xtok) launch("batch_gate_up", bx_gate_up64<TOK, 2, 2, true>, grid2, dim3(256), st, a);
+            else launch("batch_gate_up", bx_gate_up64<TOK, 2, 2>, grid2, dim3(256), st, a);
             return;
         }
+    }
+    if (a.xtok) {  // x gathered from the router's token-major split
+        if constexpr (TOK <= 16) {
+            if (tuned("bx_gate") == 2) {
+                launch("batch_gate_up", bx_gate_up<TOK, 2, 4, true>, grid, dim3(256), st, a);
+                return;
+            }
+        }
+        if (TOK == 8 || tuned("bx_gate") == 1)
+            launch("batch_gate_up", bx_gate_up<TOK, 2, 2, true>, grid, dim3(256), st, a);
+        else
+            launch("batch_gate_up", bx_gate_up<TOK, Bx<TOK>::KS, Bx<TOK>::D, true>, grid, dim3(256), st, a);
+        return;
     }
     if constexpr (TOK <= 16) {  // deeper shapes spill registers at 32 tokens and run slower
         switch (tuned("bx_gate")) {
@@ -1190,8 +1285,10 @@ void launch_gate_up(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
 
 template <int TOK>
 void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
-    const int nthreads = p.groups * (p.hpad / 32) * Bx<TOK>::NX * 64;
-    launch("batch_prep", bx_prep<TOK>, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), st, a);
+    if (!a.xtok) {
+        const int nthreads = p.groups * (p.hpad / 32) * Bx<TOK>::NX * 64;
+        launch("batch_prep", bx_prep<TOK>, dim3((unsigned)((nthreads + 255) / 256)), dim3(256), st, a);
+    }
     launch_gate_up<TOK>(p, a, st);
     const dim3 grid((unsigned)(p.groups * p.nchunks * p.nslices));
     if constexpr (TOK <= 32) {
@@ -1210,7 +1307,7 @@ void launch_tok(const BatchPlan &p, const BxArgs &a, hipStream_t st) {
 // pass's tokens.  Stats arrays are indexed from stats_base.
 ts_status run_batch(const float *x, const void *wg, const void *wu, const void *wd, size_t expert_stride,
                     const int32_t *topk, const float *topw, const BatchPlan &p, float *out,
-                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st, bool dense) {
+                    const ts_ffn_stats *stats, int stats_base, void *ws, hipStream_t st, bool dense, bool xtok) {
     BxArgs a;
     a.dense = dense ? 1 : 0;
     a.x = x;
@@ -1242,6 +1339,9 @@ ts_status run_batch(const float *x, const void *wg, const void *wu, const void *
     a.amask = ws_at<uint32_t>(ws, p.off_amask);
     a.partial = ws_at<float>(ws, p.off_partial);
     a.out = out;
+    // the router's split exists only with a routing table
+    a.xtok = (xtok && topk) ? ws_at<uint16_t>(ws, p.off_xhl) : nullptr;
+    a.xchunks = p.hpad / 8;
     const bool want_lists = stats && (stats->n_gate || stats->n_active || stats->gate_idx || stats->active_idx);
     a.want_masks = want_lists ? 1 : 0;
 

@@ -117,6 +117,19 @@ __device__ __forceinline__ f32x4 ld_f32x4_masked(const float *p, int i4, int n4)
     return i4 < n4 ? v : f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// x = hi + lo as two bf16 parts (16 significant bits together), the matrix
+// cores' operands for fp32-level products with bf16 weights.
+__device__ __forceinline__ void split_hi_lo(float x, uint32_t &hi, uint32_t &lo) {
+    hi = bf16_bits(x);
+    lo = bf16_bits(x - __uint_as_float(hi << 16));
+}
+
 __device__ __forceinline__ int lane_prefix(uint64_t mask, int lane) {
     return __popcll(mask & ((1ull << lane) - 1ull));
 }

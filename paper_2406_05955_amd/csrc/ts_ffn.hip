@@ -1794,11 +1794,15 @@ __global__ __launch_bounds__(256) void ffn_union_count(const int32_t *__restrict
 // Router of the MoE layer, one 256-thread block per token: x in registers,
 // each wave dots two expert rows at a time (all loads in flight), then
 // wave 0 takes the softmax, the top-k and the renormalised weights
-// (route_wave).
+// (route_wave).  With xs set (bf16 weights, the batched path), the block
+// also writes its token's x as bf16 high / low parts for the matrix cores:
+// row t of xs holds xs_chunks chunks of 8 values (k = 8 c .. 8 c + 7), each
+// 32 bytes (the 8 high parts, then the 8 low parts), zero past H.
 template <typename WT, int NC>
 __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, const WT *__restrict__ wr, int H,
                                                   int E, int K, int32_t *__restrict__ topk_idx,
-                                                  float *__restrict__ topk_w) {
+                                                  float *__restrict__ topk_w, uint16_t *__restrict__ xs,
+                                                  int xs_chunks) {
     constexpr int CE = WTraits<WT>::CE;
     constexpr int R = NC >= 16 ? 1 : 2;
     __shared__ float s_l[kMaxExperts];
@@ -1807,6 +1811,33 @@ __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, c
     const int nch = H / CE;
     float xr[NC][CE];
     load_x<WT, NC>(x + (size_t)t * H, lane, nch, xr);
+    if constexpr (CE == 8) {
+        if (xs) {
+            // every wave holds all of x; wave w writes the chunks c0 = w mod 4
+            u32x4 *row = reinterpret_cast<u32x4 *>(xs + (size_t)t * xs_chunks * 16);
+#pragma unroll
+            for (int c0 = 0; c0 < NC; ++c0) {
+                const int c = lane + 64 * c0;
+                if ((c0 & 3) == wave && c < nch) {
+                    uint32_t hi[4], lo[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t h0, l0, h1, l1;
+                        split_hi_lo(xr[c0][2 * e], h0, l0);
+                        split_hi_lo(xr[c0][2 * e + 1], h1, l1);
+                        hi[e] = h0 | (h1 << 16);
+                        lo[e] = l0 | (l1 << 16);
+                    }
+                    row[2 * c] = u32x4{hi[0], hi[1], hi[2], hi[3]};
+                    row[2 * c + 1] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+                }
+            }
+            for (int c = nch + (int)threadIdx.x; c < xs_chunks; c += 256) {
+                row[2 * c] = u32x4{0u, 0u, 0u, 0u};
+                row[2 * c + 1] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+    }
     for (int e = wave; e < E; e += 4 * R) {
         const WT *rows[R];
         bool valid[R];
@@ -1938,15 +1969,15 @@ ts_status launch_reduce(const float *partial, int rows, const SlotPlan &p, const
 
 template <typename WT>
 void launch_router(int nc, int batch, hipStream_t st, const float *x, const void *wr, int H, int E, int K,
-                   int32_t *ridx, float *rw) {
+                   int32_t *ridx, float *rw, uint16_t *xs = nullptr, int xs_chunks = 0) {
     const WT *w = static_cast<const WT *>(wr);
     const dim3 g((unsigned)batch), b(256);
     switch (nc) {
-    case 1: launch("moe_router", moe_router<WT, 1>, g, b, st, x, w, H, E, K, ridx, rw); break;
-    case 2: launch("moe_router", moe_router<WT, 2>, g, b, st, x, w, H, E, K, ridx, rw); break;
-    case 4: launch("moe_router", moe_router<WT, 4>, g, b, st, x, w, H, E, K, ridx, rw); break;
-    case 8: launch("moe_router", moe_router<WT, 8>, g, b, st, x, w, H, E, K, ridx, rw); break;
-    default: launch("moe_router", moe_router<WT, 16>, g, b, st, x, w, H, E, K, ridx, rw); break;
+    case 1: launch("moe_router", moe_router<WT, 1>, g, b, st, x, w, H, E, K, ridx, rw, xs, xs_chunks); break;
+    case 2: launch("moe_router", moe_router<WT, 2>, g, b, st, x, w, H, E, K, ridx, rw, xs, xs_chunks); break;
+    case 4: launch("moe_router", moe_router<WT, 4>, g, b, st, x, w, H, E, K, ridx, rw, xs, xs_chunks); break;
+    case 8: launch("moe_router", moe_router<WT, 8>, g, b, st, x, w, H, E, K, ridx, rw, xs, xs_chunks); break;
+    default: launch("moe_router", moe_router<WT, 16>, g, b, st, x, w, H, E, K, ridx, rw, xs, xs_chunks); break;
     }
 }
 
@@ -2282,14 +2313,22 @@ ts_status moe_impl(const float *x, const void *wr, const void *wg, const void *w
     const bool batched = batch > 1 && tuned("batch_path") == 0 && plan_batch(batch, hidden, inter, E, K, dt, &bp);
     // on the pipelined kernel each workgroup routes its own token (no router launch)
     const bool fold = !batched && slots_use_pipe(p, dense);
+    // batched: the router also writes each token's x split for the matrix
+    // cores, and the gate+up kernel gathers its group's tokens from it (no
+    // dispatch kernel, one copy of x in L2 for all expert groups)
+    const bool xtok = batched && tuned("bx_xtok") == 0;
     if (!fold) {
-        if (dt == TS_F32) launch_router<float>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
-        else launch_router<uint16_t>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
+        if (dt == TS_F32) {
+            launch_router<float>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw);
+        } else {
+            launch_router<uint16_t>(p.nc, batch, st, x, wr, hidden, E, K, ridx, rw,
+                                    xtok ? ws_at<uint16_t>(ws, bp.off_xhl) : nullptr, bp.hpad / 8);
+        }
         s = check_launch("moe_router");
         if (s != TS_OK) return s;
     }
     if (batched) {
-        s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st, dense);
+        s = run_batch(x, wg, wu, wd, estride, ridx, rw, bp, out, stats, 0, ws, st, dense, xtok);
     } else if (fold) {
         const RouterFold rf{wr, E, K, ridx, rw};
         s = run_slots(x, wg, wu, wd, nullptr, estride, dt, dense, p, out, rw, stats, ws, st, &rf);

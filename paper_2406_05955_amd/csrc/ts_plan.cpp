@@ -18,6 +18,7 @@ std::atomic<int> g_bx_gate{0};
 std::atomic<int> g_bx_down{0};
 std::atomic<int> g_bx_vgroup{0};
 std::atomic<int> g_interleave{0};
+std::atomic<int> g_bx_xtok{0};
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 int esize(ts_dtype dt) { return dt == TS_F32 ? 4 : 2; }
@@ -38,6 +39,7 @@ int tuned(const char *key) {
     if (std::strcmp(key, "bx_down") == 0) return g_bx_down.load();
     if (std::strcmp(key, "bx_vgroup") == 0) return g_bx_vgroup.load();
     if (std::strcmp(key, "ffn_interleave") == 0) return g_interleave.load();
+    if (std::strcmp(key, "bx_xtok") == 0) return g_bx_xtok.load();
     return 0;
 }
 
@@ -402,6 +404,11 @@ ts_status ts_tune_set(const char *key, int value) {
     if (std::strcmp(key, "ffn_interleave") == 0) {
         if (value < 0 || value > 1) return TS_ERR_SHAPE;
         ts::g_interleave.store(value);
+        return TS_OK;
+    }
+    if (std::strcmp(key, "bx_xtok") == 0) {
+        if (value < 0 || value > 1) return TS_ERR_SHAPE;
+        ts::g_bx_xtok.store(value);
         return TS_OK;
     }
     return TS_ERR_SHAPE;

@@ -183,6 +183,56 @@ def test_moe_batch_mixtral_shape(B, gate_bias):
     assert abs(frac - want) < 0.01, frac
 
 
+@pytest.mark.parametrize("B,H,I,E,K,skew,gate", [(16, 4096, 2048, 8, 2, False, 0), (2, 512, 900, 8, 2, False, 0),
+                                                 (6, 1032, 700, 8, 2, False, 0), (8, 256, 200, 64, 8, False, 0),
+                                                 (16, 1024, 1500, 8, 2, True, 0), (32, 2048, 1000, 8, 2, False, 0),
+                                                 (64, 1024, 700, 8, 2, True, 0), (40, 256, 200, 64, 8, False, 0),
+                                                 (24, 512, 333, 4, 2, False, 3), (32, 512, 300, 8, 2, False, 1),
+                                                 (16, 256, 100, 8, 2, False, 2), (64, 512, 300, 2, 2, False, 0)])
+def test_moe_gathered_x_matches_dispatch_fragments(B, H, I, E, K, skew, gate):
+    """The router also writes every token's x split once and the gate + up
+    kernels list their group's tokens and gather their columns themselves
+    (no dispatch kernel).  The operands are the dispatch kernel's fragments
+    bit for bit, so the output, the routing table, the report and the dense
+    comparator are the same bits either way, at 8, 16, 32 and 64 token
+    slots per group and with each gate + up load shape (`gate`, the bx_gate
+    knob): hidden not a multiple of 1024, 64 experts (most groups empty),
+    and (skew) a router that sends every token to experts 0 and 1, which
+    then take further groups."""
+    m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=synth.BF16, seed=[39, B, H, I, E, K])
+    if skew:
+        m.w_router[0, 0] = synth.f32_to_bf16_bits(np.float32([10.0]))[0]  # x[:, 0] = 1: a logit bias
+        m.w_router[1, 0] = synth.f32_to_bf16_bits(np.float32([9.0]))[0]
+    args = [to_dev(m.x), to_dev(m.w_router), to_dev(m.w_gate), to_dev(m.w_up), to_dev(m.w_down_t)]
+
+    def run(knob):
+        ts.tune_set("bx_xtok", knob)
+        ts.tune_set("bx_gate", gate)
+        try:
+            out, idx, w, st = ts.moe_sparse(*args, K, stats=True)
+            dense = ts.moe_dense(*args, K)[0]
+            torch.cuda.synchronize()
+            return [out.clone(), idx.clone(), w.clone(), dense.clone()], {k: v.clone() for k, v in st.items()}
+        finally:
+            ts.tune_set("bx_xtok", 0)
+            ts.tune_set("bx_gate", 0)
+    ga, sa = run(0)
+    fr, sf = run(1)
+    for a, b in zip(ga, fr):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    for k in sa:
+        if k in ("gate_idx", "active_idx"):
+            cnt = sa["n_gate" if k == "gate_idx" else "n_active"]
+            for r in range(cnt.numel()):
+                n = int(cnt[r])
+                assert torch.equal(sa[k][r, :n], sf[k][r, :n]), (k, r)
+        else:
+            assert torch.equal(sa[k], sf[k]), k
+    if skew:
+        assert (torch.sort(ga[1], dim=1).values.cpu().numpy() == [0, 1]).all()
+    moe_check(m)
+
+
 @pytest.mark.parametrize("B,H,I,E,K", [(16, 512, 1000, 1, 1), (32, 1024, 2048, 1, 1), (64, 256, 720, 1, 1),
                                        (20, 512, 33, 1, 1), (48, 2048, 1600, 8, 2), (64, 512, 900, 8, 2),
                                        (40, 256, 200, 64, 8)])
