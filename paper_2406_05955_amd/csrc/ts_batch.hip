@@ -921,11 +921,15 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     constexpr int BG = 2;          // n-tiles whose operands are read from LDS together
     constexpr int AP = 40;         // bf16 per row of the Combined tile (80 bytes: 16-row reads do not conflict)
     constexpr int HC = TOK / 8;    // 16-byte Combined chunks per lane (token half of one slot)
-    constexpr int MAXR = kBxChunkTiles * kBxRows;
+    constexpr int MAXT = bx_down_tiles(TOK);  // tiles per chunk at most
+    constexpr int MAXR = MAXT * kBxRows;       // list entries at most
+    constexpr int WPT = MAXR / 4 / 256;        // row-byte words (4 rows each) per thread
+    static_assert(MAXT <= 512 && MAXR % 1024 == 0, "two tiles per thread in the count scan; whole words per thread");
     __shared__ u32x4 s_lds[4 * REG];
-    __shared__ __attribute__((aligned(16))) uint32_t s_row[MAXR];  // listed rows (index within the group)
-    __shared__ int32_t s_hix[MAXR];                                // their Combined record, -1 = padding
-    __shared__ int s_pre[kBxChunkTiles + 1];
+    // listed rows: (tile within the chunk) << 10 | slot << 5 | row within the tile, or kPadRow
+    __shared__ __attribute__((aligned(16))) uint32_t s_ent[MAXR];
+    __shared__ int s_pre[MAXT + 1];
+    __shared__ int s_wsum[4];
     // the Combined tile: past the staging 8 KB of the wave's region when it has room (NT >= 2)
     constexpr bool AIN = NT >= 2;
     __shared__ __attribute__((aligned(16))) uint16_t s_a_own[AIN ? 1 : 4][2 * TOK][AP];
@@ -933,17 +937,21 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lm = lane & 15, lq = lane >> 4;
     // Work item (group, chunk, slice).  The dispatcher hands workgroup b to
-    // XCD b % 8; when the (group, chunk) pairs come in multiples of 8, pair p
-    // goes to XCD p % 8 with all of its slices, so the pair's Combined
+    // XCD b % 8; when the (group, chunk) pairs come in multiples of 8, each
+    // pair goes to one XCD with all of its slices, so the pair's Combined
     // fragments and row lists are fetched into one XCD's L2 only (spread
     // over all eight they were fetched eight times: 13% of the kernel's HBM
-    // reads at batch 32).  Any dispatch order gives the same results.
+    // reads at batch 32).  In round j XCD q takes pair 8 j + (q - j) mod 8:
+    // pairs that advance in steps of 2 or 8 (an expert's second, usually
+    // empty group; a group of 8 chunks) still reach every XCD.  Any
+    // dispatch order gives the same results.
     int slice, pair;
     const int npairs = a.G * a.nchunks;
     if (npairs % 8 == 0) {
         const int q = blockIdx.x % 8, r = blockIdx.x / 8;
+        const int j = r / a.nslices;
         slice = r % a.nslices;
-        pair = (r / a.nslices) * 8 + q;
+        pair = 8 * j + ((q - j) & 7);
     } else {
         slice = blockIdx.x % a.nslices;
         pair = blockIdx.x / a.nslices;
@@ -958,24 +966,35 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     const size_t tbase = (size_t)g * a.ntiles + t0;
 
     // ---- the chunk's row list: the tiles' counts and row bytes are read in
-    // one round trip (bx_gate_up writes all 32 row bytes of a tile) ---------
-    constexpr int EPT = MAXR / 256;  // tile entries per thread
-    uint32_t rbv[EPT];
+    // one round trip (bx_gate_up writes all 32 row bytes of a tile, 8 words)
+    uint32_t rbw[WPT];
+    const uint32_t *arow32 = reinterpret_cast<const uint32_t *>(a.arow) + tbase * (kBxRows / 4);
 #pragma unroll
-    for (int u = 0; u < EPT; ++u) {
-        const int e = tid + 256 * u;
-        rbv[u] = e < ntc * kBxRows ? a.arow[tbase * kBxRows + e] : 0u;
+    for (int u = 0; u < WPT; ++u) {
+        const int w = tid + 256 * u;
+        rbw[u] = w < ntc * (kBxRows / 4) ? arow32[w] : 0u;
     }
-    if (wave == 0) {
-        const int na = lane < ntc ? a.cnt[(tbase + lane) * 2 + 1] : 0;
-        int inc = na;
+    // exclusive prefix of the active counts: thread i holds tiles 2i, 2i + 1
+    const int ta = 2 * tid;
+    const int na_a = ta < ntc ? a.cnt[(tbase + ta) * 2 + 1] : 0;
+    const int na_b = ta + 1 < ntc ? a.cnt[(tbase + ta + 1) * 2 + 1] : 0;
+    {
+        const int v = na_a + na_b;
+        int inc = v;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
-            const int v = __shfl_up(inc, o, 64);
-            if (lane >= o) inc += v;
+            const int t = __shfl_up(inc, o, 64);
+            if (lane >= o) inc += t;
         }
-        if (lane < ntc) s_pre[lane] = inc - na;
-        if (lane == 63) s_pre[ntc] = inc;
+        if (lane == 63) s_wsum[wave] = inc;
+        __syncthreads();
+        int before = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) before += w < wave ? s_wsum[w] : 0;
+        const int ex = before + inc - v;
+        if (ta < ntc) s_pre[ta] = ex;
+        if (ta + 1 < ntc) s_pre[ta + 1] = ex + na_a;
+        if (tid == 255) s_pre[ntc] = ex + v;
     }
     __syncthreads();
     const int total = s_pre[ntc];
@@ -983,21 +1002,19 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
     // listed rows; the block padding past `total` loads at an out-of-range
     // offset (zeros, no traffic) and has zero Combined
 #pragma unroll
-    for (int u = 0; u < EPT; ++u) {
-        const int e = tid + 256 * u;
-        if (e < ntc * kBxRows) {
-            const int t = e / kBxRows, sl = e - t * kBxRows;
-            const int base = s_pre[t];
-            if (sl < s_pre[t + 1] - base) {
-                s_row[base + sl] = (uint32_t)((t0 + t) * kBxRows) + rbv[u];
-                s_hix[base + sl] = (int32_t)((tbase + t) * kBxRows + sl);
-            }
-        }
-        if (e >= total && e < nblk * kBxRows) {
-            s_row[e] = kPadRow;
-            s_hix[e] = -1;
+    for (int u = 0; u < WPT; ++u) {
+        const int w = tid + 256 * u;
+        if (w < ntc * (kBxRows / 4)) {
+            const int t = w / (kBxRows / 4), s4 = 4 * (w % (kBxRows / 4));
+            const int base = s_pre[t], na = s_pre[t + 1] - base;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (s4 + j < na)
+                    s_ent[base + s4 + j] =
+                        ((uint32_t)t << 10) | ((uint32_t)(s4 + j) << 5) | ((rbw[u] >> (8 * j)) & 31u);
         }
     }
+    for (int e = total + tid; e < nblk * kBxRows; e += 256) s_ent[e] = kPadRow;
     __syncthreads();
 
     const uint16_t *wde = reinterpret_cast<const uint16_t *>(a.wd) + (size_t)(g / a.vpe) * a.expert_stride;
@@ -1024,15 +1041,18 @@ __global__ __launch_bounds__(256, TOK <= 16 ? 2 : 1) void bx_down(BxArgs a) {
         auto issue = [&](int d) {
             const int bb = kk < nbw ? wave + 4 * kk : wave;
             ++kk;
-            const u32x4 ra = *reinterpret_cast<const u32x4 *>(&s_row[bb * kBxRows + 8 * lq]);
-            const u32x4 rb = *reinterpret_cast<const u32x4 *>(&s_row[bb * kBxRows + 8 * lq + 4]);
+            const u32x4 ra = *reinterpret_cast<const u32x4 *>(&s_ent[bb * kBxRows + 8 * lq]);
+            const u32x4 rb = *reinterpret_cast<const u32x4 *>(&s_ent[bb * kBxRows + 8 * lq + 4]);
             const uint32_t rr[8] = {ra.x, ra.y, ra.z, ra.w, rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                wv[d][q] = ld_buf_stream(rwd, rr[q] == kPadRow ? kOutOfRange : rr[q] * H2 + cw);
-            const int hx = s_hix[bb * kBxRows + hj];
-            hok[d] = hx >= 0;
-            const uint16_t *hs = a.hfrag + (size_t)(hx >= 0 ? hx : 0) * (2 * TOK) + hh * TOK;
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t row = (uint32_t)(t0 + (int)(rr[q] >> 10)) * kBxRows + (rr[q] & 31u);
+                wv[d][q] = ld_buf_stream(rwd, rr[q] == kPadRow ? kOutOfRange : row * H2 + cw);
+            }
+            const uint32_t he = s_ent[bb * kBxRows + hj];
+            hok[d] = he != kPadRow;
+            const size_t hx = hok[d] ? (tbase + (he >> 10)) * kBxRows + ((he >> 5) & 31u) : 0;
+            const uint16_t *hs = a.hfrag + hx * (2 * TOK) + hh * TOK;
 #pragma unroll
             for (int c = 0; c < HC; ++c) hq[d][c] = ld_cached(hs + 8 * c);
         };

@@ -224,7 +224,7 @@ bool plan_batch(int batch, int hidden, int inter, int experts, int top_k, ts_dty
     int want = g_down_chunks.load();
     if (want <= 0) want = std::max(1, 256 / (q.nslices * groups));
     q.nchunks = std::max(1, std::min(want, q.ntiles));
-    q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, kBxChunkTiles);
+    q.tpc = std::min((q.ntiles + q.nchunks - 1) / q.nchunks, bx_down_tiles(q.tok));
     q.nchunks = (q.ntiles + q.tpc - 1) / q.tpc;
     const size_t G = (size_t)groups, T = (size_t)q.ntiles;
     size_t off = 0;

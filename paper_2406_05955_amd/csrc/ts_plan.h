@@ -86,7 +86,15 @@ struct SlotPlan {
 constexpr int kBxMaxTokens = 64;  // tokens per group and pass
 constexpr int kBxRows = 32;       // neurons per gate+up workgroup tile (and per down K block)
 constexpr int kBxSliceCols = 128; // output columns per down wave
-constexpr int kBxChunkTiles = 64; // gate+up tiles per down chunk (one wave ballot)
+// gate+up tiles per down workgroup at most: its row list (4 bytes per
+// entry, room for every row of every tile) lives in LDS next to the
+// staging.  At 32 token slots a compute unit holds one workgroup whatever
+// the list, so a workgroup takes up to 448 tiles (a whole 14336-neuron
+// expert: one round of workgroups instead of seven, MoE batch 64 down 112
+// -> 89 us); at 8 and 16, 64 tiles (shorter workgroups, three or two per
+// unit, measured faster than 96- or 224-tile ones at 85% in-expert
+// sparsity); at 64 the staging leaves room for 64.
+constexpr int bx_down_tiles(int tok) { return tok == 32 ? 448 : 64; }
 constexpr int kBxKQuant = 1024;   // the hidden dimension is padded to this (4 waves x 2 batches x 128)
 
 // A "group" is one weight set with up to `tok` of its tokens.  The FFN has
@@ -105,7 +113,7 @@ struct BatchPlan {
     int ntiles = 0;      // 32-neuron tiles per group
     int nslices = 0;     // 128-column slices of the down kernel
     int nchunks = 0;     // tile chunks per group in the down kernel
-    int tpc = 0;         // tiles per chunk (<= kBxChunkTiles)
+    int tpc = 0;         // tiles per chunk (<= bx_down_tiles(tok))
     size_t off_gcount = 0, off_tslot = 0, off_xhl = 0, off_cnt = 0, off_arow = 0, off_hfrag = 0;
     size_t off_gmask = 0, off_amask = 0, off_partial = 0, off_union = 0;
     size_t total = 0;
