@@ -896,8 +896,9 @@ __global__ __launch_bounds__(256, TOK >= 64 ? 1 : 2) void bx_gate_up64(BxArgs a)
 // ---------------------------------------------------------------------------
 // Down: workgroup (group, chunk of tiles, 128-column slice), 4 waves.  The
 // chunk's active rows, tile after tile in ascending order, are listed once
-// in LDS (row, and where its Combined values are) and cut into K blocks of
-// 32; wave w takes blocks w, w + 4, ...  A block's W_down_t rows x the
+// in LDS (4 bytes each: the tile within the chunk, the slot of its Combined
+// record, the row within the tile; up to bx_down_tiles(TOK) tiles) and cut
+// into K blocks of 32; wave w takes blocks w, w + 4, ...  A block's W_down_t rows x the
 // slice's 128 columns (8 KB) are loaded as 8 coalesced 16-byte loads per
 // lane (lane (lq, lm): slot 8 lq + q, columns 8 lm .. 8 lm + 7) and written
 // to the wave's own LDS region row-major, the 16-byte chunk c of slot s at
