@@ -84,6 +84,58 @@ int main() {
     ts_tune_set("gate_tile", 0);
     ts_tune_set("down_chunks", 0);
     ts_tune_set("ffn_tile", 0);
+
+    // the batched (matrix-core) plan: token slots per group, groups per
+    // weight set, the down kernel's chunks within its row list, and the
+    // workspace regions the kernels index (the x region also holds the
+    // router's token-major x split: batch x hpad x 4 bytes)
+    const int Bs[] = {2, 3, 8, 9, 16, 17, 32, 33, 48, 64};
+    const int Es[] = {1, 2, 3, 8, 64};
+    for (int vg : {0, 1})
+        for (int dc : {0, 7, 14})
+            for (int B : Bs)
+                for (int E : Es)
+                    for (int K : {1, 2, 8})
+                        for (int H : {8, 200, 1032, 4096, 8192})
+                            for (int I : {1, 33, 700, 14336, 14368}) {
+                                if (K > E) continue;
+                                ts_tune_set("bx_vgroup", vg);
+                                ts_tune_set("down_chunks", dc);
+                                BatchPlan p;
+                                if (!plan_batch(B, H, I, E, K, TS_BF16, &p)) return fail("batch plan refused", B, H, I, E);
+                                if (plan_batch(B, H, I, E, K, TS_F32, &p)) return fail("batch plan fp32", B, H, I, E);
+                                plan_batch(B, H, I, E, K, TS_BF16, &p);
+                                const int want = (E > 1 && vg == 0) ? std::min(B, 2 * ((B * K + E - 1) / E)) : B;
+                                if (p.tok != 8 && p.tok != 16 && p.tok != 32 && p.tok != 64) return fail("tok", B, H, I, E);
+                                if (p.tok < want || (p.tok > 8 && p.tok / 2 >= want)) return fail("tok size", B, H, I, E);
+                                if ((long long)p.vpe * p.tok < B || p.groups != E * p.vpe) return fail("groups", B, H, I, E);
+                                if (p.hpad < H || p.hpad % kBxKQuant) return fail("hpad", B, H, I, E);
+                                if (p.ntiles != (I + kBxRows - 1) / kBxRows) return fail("ntiles", B, H, I, E);
+                                if (p.nslices != (H + kBxSliceCols - 1) / kBxSliceCols) return fail("nslices", B, H, I, E);
+                                if (p.tpc < 1 || p.tpc > bx_down_tiles(p.tok)) return fail("down chunk", B, H, I, E);
+                                if ((long long)p.nchunks * p.tpc < p.ntiles || (long long)(p.nchunks - 1) * p.tpc >= p.ntiles)
+                                    return fail("down chunks cover", B, H, I, E);
+                                const size_t G = (size_t)p.groups, T = (size_t)p.ntiles;
+                                const size_t offs[] = {p.off_gcount, p.off_tslot, p.off_xhl, p.off_cnt, p.off_arow,
+                                                       p.off_hfrag, p.off_gmask, p.off_amask, p.off_partial,
+                                                       p.off_union, p.total};
+                                for (size_t k = 0; k + 1 < sizeof(offs) / sizeof(offs[0]); ++k)
+                                    if (offs[k] % 256 || offs[k + 1] < offs[k]) return fail("batch offsets", B, H, I, E);
+                                if (p.off_tslot - p.off_gcount < G * 4) return fail("gcount size", B, H, I, E);
+                                if (p.off_xhl - p.off_tslot < (size_t)B * K * 8) return fail("tslot size", B, H, I, E);
+                                const size_t xfrag = G * 2 * p.tok * p.hpad * 2, xtok = (size_t)B * p.hpad * 4;
+                                if (p.off_cnt - p.off_xhl < std::max(xfrag, xtok)) return fail("x region", B, H, I, E);
+                                if (p.off_arow - p.off_cnt < G * T * 8) return fail("cnt size", B, H, I, E);
+                                if (p.off_hfrag - p.off_arow < G * T * kBxRows) return fail("arow size", B, H, I, E);
+                                if (p.off_gmask - p.off_hfrag < G * T * 2 * p.tok * kBxRows * 2) return fail("hfrag size", B, H, I, E);
+                                if (p.off_partial - p.off_amask < G * T * p.tok * 4) return fail("amask size", B, H, I, E);
+                                if (p.off_union - p.off_partial < G * p.tok * (size_t)p.nchunks * H * 4)
+                                    return fail("partial size", B, H, I, E);
+                            }
+    ts_tune_set("bx_vgroup", 0);
+    ts_tune_set("down_chunks", 0);
+    BatchPlan q;
+    if (plan_batch(65, 4096, 14336, 8, 2, TS_BF16, &q)) return fail("batch above 64", 65, 4096, 14336, 8);
     std::printf("ok\n");
     return 0;
 }
