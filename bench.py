@@ -30,6 +30,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import glob
 import hashlib
 import json
 import os
@@ -41,8 +42,13 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 H_MISTRAL, I_MISTRAL = 4096, 14336
-KERNEL_SOURCES = ["paper_2406_05955_amd/csrc/ts_ffn.hip", "paper_2406_05955_amd/csrc/ts_device.h",
-                  "paper_2406_05955_amd/csrc/ts_plan.cpp", "paper_2406_05955_amd/csrc/ts_plan.h"]
+# Every source the library is built from: a profile summary stamped with
+# another hash was taken on other code, whichever kernel changed.
+KERNEL_SOURCES = sorted(
+    os.path.relpath(p, ROOT)
+    for ext in ("*.hip", "*.h", "*.cpp")
+    for p in glob.glob(os.path.join(ROOT, "paper_2406_05955_amd", "csrc", ext))) + [
+        "paper_2406_05955_amd/build.py", "include/turbosparse.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_ffn_main_mistral_b1.txt")
 TRACE_FILE = os.path.join(ROOT, "profiles", "trace_ffn_main_mistral_b1.txt")
 

@@ -43,7 +43,9 @@ def test_kernel_hash_covers_the_kernel_sources():
     assert len(b.kernel_hash()) == 16
     for p in b.KERNEL_SOURCES:
         assert os.path.exists(os.path.join(ROOT, p)), p
-    assert any(p.endswith("ts_ffn.hip") for p in b.KERNEL_SOURCES)
+    for name in ("ts_ffn.hip", "ts_batch.hip", "ts_batch.h", "ts_device.h", "ts_plan.cpp", "ts_plan.h",
+                 "ts_runtime.cpp", "ts_probe.hip", "build.py", "turbosparse.h"):
+        assert any(p.endswith(name) for p in b.KERNEL_SOURCES), name
 
 
 def test_algorithmic_bytes():
