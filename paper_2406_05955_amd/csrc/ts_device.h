@@ -111,6 +111,12 @@ __device__ __forceinline__ u32x4 ld_buf_stream(__amdgpu_buffer_rsrc_t r, uint32_
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
 }
 
+// The same with the default cache policy: for data that many workgroups
+// read (it stays in L2 for the ones after the first).
+__device__ __forceinline__ u32x4 ld_buf_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
 __device__ __forceinline__ f32x4 ld_f32x4_masked(const float *p, int i4, int n4) {
     const int ii = i4 < n4 ? i4 : n4 - 1;
     f32x4 v = *reinterpret_cast<const f32x4 *>(p + (size_t)ii * 4);

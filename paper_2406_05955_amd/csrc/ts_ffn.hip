@@ -476,16 +476,22 @@ __global__ __launch_bounds__(kThreads) void ffn_pipe(SlotArgs a) {
     if (a.route) {
         eoff = (size_t)a.route[slot] * a.expert_stride;
     } else if (a.wr) {
-        // the token's router: wave w dots expert rows w, w + 8, ...; wave 0
-        // takes the softmax and top-k and picks this slot's expert
+        // the token's router: wave w dots expert rows (w + b) mod E,
+        // (w + 8 + b) mod E, ... for workgroup b, so that the workgroups
+        // starting together ask for different rows first, through the
+        // default cache policy (every workgroup reads the same rows); the
+        // two together measured 2% faster per layer than every workgroup's
+        // wave w on row w with streaming loads; wave 0 takes the softmax and
+        // top-k and picks this slot's expert
         const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.wr, (uint32_t)a.E * (uint32_t)H * (uint32_t)sizeof(WT));
-        for (int e = wave; e < a.E; e += kWaves) {
+        for (int i = wave; i < a.E; i += kWaves) {
+            const int e = (i + (int)(blockIdx.x % (unsigned)a.E)) % a.E;
             u32x4 v[NC];
             const uint32_t base = (uint32_t)e * (uint32_t)H * (uint32_t)sizeof(WT);
 #pragma unroll
             for (int c0 = 0; c0 < NC; ++c0) {
                 const int c = lane + 64 * c0;
-                v[c0] = ld_buf_stream(rr, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
+                v[c0] = ld_buf_cached(rr, c < nch ? base + (uint32_t)c * 16u : kOutOfRange);
             }
             float d = 0.f;
 #pragma unroll
