@@ -89,6 +89,14 @@ __device__ __forceinline__ u32x4 ld_stream_masked(const void *row, int c, int nc
     return keep ? v : u32x4{0u, 0u, 0u, 0u};
 }
 
+// ld_stream_masked with the default cache policy (rows many workgroups read).
+__device__ __forceinline__ u32x4 ld_cached_masked(const void *row, int c, int nch, int bytes_per_chunk, bool ok) {
+    const int cc = c < nch ? c : nch - 1;
+    u32x4 v = ld_cached(static_cast<const char *>(row) + (size_t)cc * bytes_per_chunk);
+    const bool keep = ok && c < nch;
+    return keep ? v : u32x4{0u, 0u, 0u, 0u};
+}
+
 // Same without the mask: chunks past the row end re-read its last chunk.
 // Callers pair such chunks with zero x values, so they add nothing.
 __device__ __forceinline__ u32x4 ld_stream_clamped(const void *row, int c, int nch) {

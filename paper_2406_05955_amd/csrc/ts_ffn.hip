@@ -86,8 +86,9 @@ __device__ __forceinline__ void load_x(const float *__restrict__ x, int lane, in
 // Dot products of R weight rows with the x chunks held in registers.  All
 // R * NC loads are issued before any arithmetic; rows with valid[k] false
 // (and chunks past the row end) read a clamped address and count as zero.
-// Returns wave-uniform sums.
-template <typename WT, int NC, int R>
+// Streaming loads, or (CACHED) the default cache policy for rows that many
+// workgroups read.  Returns wave-uniform sums.
+template <typename WT, int NC, int R, bool CACHED = false>
 __device__ __forceinline__ void dot_rows(const WT *const (&rows)[R], const bool (&valid)[R],
                                          const float (&xr)[NC][WTraits<WT>::CE], int lane, int nch,
                                          float (&out)[R]) {
@@ -96,7 +97,10 @@ __device__ __forceinline__ void dot_rows(const WT *const (&rows)[R], const bool 
 #pragma unroll
     for (int k = 0; k < R; ++k)
 #pragma unroll
-        for (int c0 = 0; c0 < NC; ++c0) v[k][c0] = ld_stream_masked(rows[k], lane + 64 * c0, nch, 16, valid[k]);
+        for (int c0 = 0; c0 < NC; ++c0) {
+            if constexpr (CACHED) v[k][c0] = ld_cached_masked(rows[k], lane + 64 * c0, nch, 16, valid[k]);
+            else v[k][c0] = ld_stream_masked(rows[k], lane + 64 * c0, nch, 16, valid[k]);
+        }
 #pragma unroll
     for (int k = 0; k < R; ++k) {
         float d = 0.f;
@@ -1844,20 +1848,26 @@ __global__ __launch_bounds__(256) void moe_router(const float *__restrict__ x, c
             }
         }
     }
+    // every block reads all router rows: cached loads, and the blocks that
+    // start together begin at different rows (block t's wave w takes rows
+    // (w + t) mod E, (w + 4 + t) mod E, ...; measured 1-1.5 us shorter)
+    const int rot = (int)(blockIdx.x % (unsigned)E);
     for (int e = wave; e < E; e += 4 * R) {
         const WT *rows[R];
         bool valid[R];
+        int ex[R];
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             valid[k] = e + 4 * k < E;
-            rows[k] = wr + (size_t)(valid[k] ? e + 4 * k : e) * H;
+            ex[k] = ((valid[k] ? e + 4 * k : e) + rot) % E;
+            rows[k] = wr + (size_t)ex[k] * H;
         }
         float d[R];
-        dot_rows<WT, NC, R>(rows, valid, xr, lane, nch, d);
+        dot_rows<WT, NC, R, true>(rows, valid, xr, lane, nch, d);
         if (lane == 0) {
 #pragma unroll
             for (int k = 0; k < R; ++k)
-                if (valid[k]) s_l[e + 4 * k] = d[k];
+                if (valid[k]) s_l[ex[k]] = d[k];
         }
     }
     __syncthreads();
