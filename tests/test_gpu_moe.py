@@ -68,7 +68,11 @@ def check_moe(m, dense=False):
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 @pytest.mark.parametrize("B,H,I,E,K", [(1, 512, 1024, 8, 2), (16, 512, 700, 8, 2), (3, 256, 130, 4, 4),
                                        (2, 1024, 333, 1, 1), (5, 640, 256, 64, 8), (1, 4096, 2048, 8, 2),
-                                       (256, 128, 64, 8, 2)])  # the largest batch
+                                       (256, 128, 64, 8, 2),  # the largest batch
+                                       # expert counts that do not divide the 8 waves or exceed
+                                       # them (both routers read the rows in a rotated order)
+                                       (1, 512, 700, 6, 3), (1, 384, 300, 12, 2), (9, 512, 500, 3, 2),
+                                       (12, 256, 200, 12, 3)])
 def test_moe_shapes(dtype, B, H, I, E, K):
     m = synth.make_moe(B, H, I, E, K, gate_bias=-1.5548, dtype=dtype, seed=[B, H, I, E, K])
     check_moe(m)
