@@ -71,9 +71,18 @@ def check(inp, frac):
     for t in range(B):
         c = combined(ref, t)
         want_k = kept_mask(c, keep)
-        assert int(st["n_active"][t]) == int(nk[t]) == np.count_nonzero(want_k)
-        assert compare_sets(list_of(st, "active_idx", t, "n_active"), want_k, np.ones(I, bool)) == 0
         near = np.abs(ref.g[t]) < thr
+        # neurons whose activity the two sides may decide differently (a
+        # gate, or an open gate's up, in the rounding band): when keep
+        # reaches into them, the kept sets may differ by those neurons alone
+        near_a = near | ((ref.g[t] > 0) & (np.abs(ref.u[t]) < thr))
+        assert int(st["n_active"][t]) == int(nk[t])
+        if near_a.any():
+            assert abs(int(nk[t]) - np.count_nonzero(want_k)) <= np.count_nonzero(near_a)
+            assert compare_sets(list_of(st, "active_idx", t, "n_active"), want_k, ~near_a) == 0
+        else:
+            assert int(nk[t]) == np.count_nonzero(want_k)
+            assert compare_sets(list_of(st, "active_idx", t, "n_active"), want_k, np.ones(I, bool)) == 0
         assert compare_sets(list_of(st, "gate_idx", t, "n_gate"), ref.g[t] > 0, ~near) == 0
     return out, ref, keep
 
