@@ -89,12 +89,14 @@ constexpr int kBxSliceCols = 128; // output columns per down wave
 // gate+up tiles per down workgroup at most: its row list (4 bytes per
 // entry, room for every row of every tile) lives in LDS next to the
 // staging.  At 32 token slots a compute unit holds one workgroup whatever
-// the list, so a workgroup takes up to 448 tiles (a whole 14336-neuron
-// expert: one round of workgroups instead of seven, MoE batch 64 down 112
-// -> 89 us); at 8 and 16, 64 tiles (shorter workgroups, three or two per
-// unit, measured faster than 96- or 224-tile ones at 85% in-expert
-// sparsity); at 64 the staging leaves room for 64.
-constexpr int bx_down_tiles(int tok) { return tok == 32 ? 448 : 64; }
+// the list, so a workgroup takes up to 224 tiles (half a 14336-neuron
+// expert: two rounds of workgroups instead of fourteen, MoE batch 64 down
+// 112 -> 86 us; whole experts, one round, 89 us: the experts drawing the
+// most tokens set that round's length; 160 or 128 tiles 92-93 us); at 8
+// and 16, 64 tiles (shorter workgroups, three or two per unit, measured
+// faster than 96- or 224-tile ones at 85% in-expert sparsity); at 64 the
+// staging leaves room for 64.
+constexpr int bx_down_tiles(int tok) { return tok == 32 ? 224 : 64; }
 constexpr int kBxKQuant = 1024;   // the hidden dimension is padded to this (4 waves x 2 batches x 128)
 
 // A "group" is one weight set with up to `tok` of its tokens.  The FFN has

@@ -101,11 +101,11 @@ def test_moe_mixtral_shape_b1(gate_bias, sparsity):
 
 @pytest.mark.parametrize("I", [14336, 14368])
 @pytest.mark.parametrize("dense", [True, False])
-def test_moe_whole_expert_down_lists(I, dense):
+def test_moe_long_down_lists(I, dense):
     """At 32 token slots per expert group (batch 64 over 8 experts, top 2) a
-    down workgroup lists a whole expert's active rows at once (up to 448
-    tiles of 32).  The dense comparator makes every row active, so a
-    14336-neuron expert fills that list exactly and 14368 neurons take a
-    second, one-tile set; the sparse layer at the same shapes alongside."""
+    down workgroup lists the active rows of up to 224 tiles of 32 (half a
+    14336-neuron expert) at once.  The dense comparator makes every row
+    active, so such an expert fills two lists exactly and 14368 neurons take
+    a third, one-tile list; the sparse layer at the same shapes alongside."""
     m = synth.make_moe(64, 256, I, 8, 2, gate_bias=-1.5548, dtype=synth.BF16, seed=[13, I])
     check_moe(m, dense=dense)
