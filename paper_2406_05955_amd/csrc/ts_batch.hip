@@ -137,17 +137,6 @@ __device__ __forceinline__ BxX<Bx<TOK>::NX> bx_xsource(const BxArgs &a, int g, i
     return xs;
 }
 
-// Group at grid position gi (gate / up and down kernels): every weight
-// set's first group before any further one.  An expert's further groups
-// take the tokens past its first `tok` and are nearly always empty; their
-// workgroups, which only find that out and exit, then come at the end of
-// the grid instead of between the working ones (MoE batch 16: 223 against
-// 227 us per layer).  A bijection on [0, G), G = weight sets x vpe.
-__device__ __forceinline__ int bx_group_at(int gi, int G, int vpe) {
-    const int E = G / vpe;
-    return (gi % E) * vpe + gi / E;
-}
-
 // Group g's token list (MoE): the tokens routed to expert g / vpe, entries
 // [r0, r0 + TOK) of that expert's ascending list, by one wave scanning the
 // (token, rank) pairs in token-major order; s_tok[slot] = token, -1 past the

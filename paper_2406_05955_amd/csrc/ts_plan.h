@@ -97,6 +97,15 @@ constexpr int kBxSliceCols = 128; // output columns per down wave
 // faster than 96- or 224-tile ones at 85% in-expert sparsity); at 64 the
 // staging leaves room for 64.
 constexpr int bx_down_tiles(int tok) { return tok == 32 ? 224 : 64; }
+
+// Group at grid position gi of the batched gate / up and down grids: every
+// weight set's first group before any further one.  An expert's further
+// groups take the tokens past its first `tok` and are nearly always empty;
+// their workgroups, which only find that out and exit, then come at the end
+// of the grid instead of between the working ones (MoE batch 16: 223
+// against 227 us per layer).  A bijection on [0, G) for G = weight sets x
+// vpe, which plan_batch guarantees.
+constexpr int bx_group_at(int gi, int G, int vpe) { return (gi % (G / vpe)) * vpe + gi / (G / vpe); }
 constexpr int kBxKQuant = 1024;   // the hidden dimension is padded to this (4 waves x 2 batches x 128)
 
 // A "group" is one weight set with up to `tok` of its tokens.  The FFN has

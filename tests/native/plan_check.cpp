@@ -3,6 +3,7 @@
 // the first violated invariant.
 #include <algorithm>
 #include <cstdio>
+#include <vector>
 
 #include "ts_plan.h"
 
@@ -109,6 +110,16 @@ int main() {
                                 if (p.tok != 8 && p.tok != 16 && p.tok != 32 && p.tok != 64) return fail("tok", B, H, I, E);
                                 if (p.tok < want || (p.tok > 8 && p.tok / 2 >= want)) return fail("tok size", B, H, I, E);
                                 if ((long long)p.vpe * p.tok < B || p.groups != E * p.vpe) return fail("groups", B, H, I, E);
+                                {
+                                    // the kernels' grid order of the groups: a permutation, first groups first
+                                    std::vector<char> seen((size_t)p.groups, 0);
+                                    for (int gi = 0; gi < p.groups; ++gi) {
+                                        const int g = bx_group_at(gi, p.groups, p.vpe);
+                                        if (g < 0 || g >= p.groups || seen[(size_t)g]) return fail("group order", B, H, I, E);
+                                        seen[(size_t)g] = 1;
+                                        if ((gi < E) != (g % p.vpe == 0)) return fail("group order first", B, H, I, E);
+                                    }
+                                }
                                 if (p.hpad < H || p.hpad % kBxKQuant) return fail("hpad", B, H, I, E);
                                 if (p.ntiles != (I + kBxRows - 1) / kBxRows) return fail("ntiles", B, H, I, E);
                                 if (p.nslices != (H + kBxSliceCols - 1) / kBxSliceCols) return fail("nslices", B, H, I, E);
